@@ -1,0 +1,211 @@
+"""Throughput of one Early-Bird denoising step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+A step is eb_decode_step over one batch of synthetic, seeded input already resident in HBM:
+block attention over the cached prefix + block keys, the fused LM head with its
+softmax / entropy / confidence / argmax reduction, and threshold unmasking in every block.
+Prints ONE JSON line: positions/s = block positions / step time, the roofline of the fused
+LM-head kernel (timed with hipEvents recorded by the library around that kernel), and the
+fp64 CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "block positions scored+unmasked/sec per denoising step; % HBM or MFMA peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+MFMA_F32_PEAK_TFLOPS = 157.3    # fp32 vector peak (the fp32 path uses plain FMA)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lmhead_traffic.json")
+LMHEAD_SOURCES = [os.path.join(ROOT, "paper_2609_16450_amd", "csrc", f)
+                  for f in ("lmhead.hip", "eb_common.hpp")]
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def lmhead_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in LMHEAD_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def lmhead_work(cfg, T: int):
+    """Algorithmic bytes and flops of one fused LM-head launch: W and h read once, 12 B of
+    results per row (kappa, entropy, argmax); the logits are never written."""
+    e = 4 if cfg.dtype == "f32" else 2
+    nbytes = cfg.vocab * cfg.hidden * e + T * cfg.hidden * e + 12 * T
+    flops = 2.0 * T * cfg.hidden * cfg.vocab
+    return nbytes, flops
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from rocprofv3 counters, if taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(workload)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_hash") != lmhead_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(case, budget_s: float = 15.0):
+    """Time the fp64 oracle (as it stands) on a bounded sample of the workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    from workloads import bf16_bits_to_f32
+
+    threads = max(1, min(16, os.cpu_count() or 1))
+    f = (lambda x: bf16_bits_to_f32(x)) if case.dtype == "bf16" else (lambda x: np.asarray(x))
+    # sample: whole blocks from the front of the batch, at most 64 block positions
+    nb, rows = 0, 0
+    while nb < case.batch and (rows == 0 or rows + int(case.block_lens[nb]) <= 64):
+        rows += int(case.block_lens[nb])
+        nb += 1
+    cu_b = case.cu_block[:nb + 1]
+    cu_p = case.cu_prefix[:nb + 1]
+    T, S = int(cu_b[-1]), int(cu_p[-1])
+    w = f(case.w)
+    args = (f(case.q[:T]), f(case.k_blk[:T]), f(case.v_blk[:T]), f(case.k_pre[:S]),
+            f(case.v_pre[:S]), cu_b, cu_p, case.cfg.hq, case.cfg.hkv, f(case.h[:T]), w,
+            case.masked[:T], case.tokens[:T], case.tau[:nb])
+    reps, t_total = 0, 0.0
+    with threadpool_limits(limits=threads):
+        while t_total < budget_s and reps < 50:
+            t0 = time.perf_counter()
+            oracle.decode_step(*args)
+            t_total += time.perf_counter() - t0
+            reps += 1
+    return {"value": reps * T / t_total, "unit": "positions/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} x oracle decode_step over the first {nb} block(s) ({T} block "
+                      f"positions, full vocabulary {case.cfg.vocab}, prefix {S}), fp64 numpy, "
+                      f"{t_total:.1f} s on {platform.processor() or platform.machine()}"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llada8b_b1")
+    ap.add_argument("--copies", type=int, default=2, help="input copies rotated between steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the step is built and timed on a single MI355X "
+              "(sharding across GPUs is a design note, not part of this build).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2609_16450_amd as eb
+    from paper_2609_16450_amd.binding import eb_step_trace
+    from paper_2609_16450_amd.device_case import DeviceStep
+    from workloads import CONFIGS, make_step
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    eb.load()
+    cfg = CONFIGS[args.workload]
+    log(f"bench: generating {cfg.name}")
+    case = make_step(cfg)
+    T = case.T
+    copies = [DeviceStep(case, device="cuda:0") for _ in range(max(1, args.copies))]
+    stream = torch.cuda.current_stream()
+    log(f"bench: T={T} S={case.S} warmup={args.warmup} steps={args.steps}")
+
+    def run(i, trace=None):
+        ds = copies[i % len(copies)]
+        eb.eb_decode_step(ds.buffers, stream=stream, trace=trace)
+
+    for i in range(args.warmup):
+        run(i)
+    torch.cuda.synchronize()
+
+    # headline: K whole steps, host clock between two synchronisations
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        run(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ms_events = ev0.elapsed_time(ev1) / args.steps
+    log(f"bench: {ms_per_step:.4f} ms/step (events {ms_events:.4f})")
+
+    # roofline: the same steps again with hipEvents recorded around the fused LM-head kernel
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in evs:            # create the events
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        run(i, eb_step_trace(0, 0, a.cuda_event, b.cuda_event, 0, 0))
+    torch.cuda.synchronize()
+    lm_ms = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+    nbytes, flops = lmhead_work(cfg, T)
+    ai = flops / nbytes
+    if cfg.dtype == "f32":
+        bound, peak, unit, achieved = "alu", MFMA_F32_PEAK_TFLOPS, "TFLOP/s", flops / (lm_ms * 1e-3) / 1e12
+    elif ai < (MFMA_BF16_PEAK_TFLOPS * 1e12) / (HBM_PEAK_GBS * 1e9):
+        bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", nbytes / (lm_ms * 1e-3) / 1e9
+    else:
+        bound, peak, unit, achieved = "mfma", MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", flops / (lm_ms * 1e-3) / 1e12
+    log(f"bench: fused LM-head kernel {lm_ms * 1e3:.1f} us, {achieved:.1f} {unit}")
+
+    result = {
+        "metric": METRIC,
+        "value": T / (ms_per_step * 1e-3),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": cfg.batch, "block_positions": T,
+                   "prefix_positions": case.S, "heads": f"{cfg.hq}/{cfg.hkv}x{cfg.head_dim}",
+                   "hidden": cfg.hidden, "vocab": cfg.vocab, "input_copies": len(copies),
+                   "ms_per_step_events": ms_events},
+        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+                     "frac": achieved / peak, "traffic": measured_traffic(cfg.name),
+                     "kernel": "lmhead_bf16_kernel" if cfg.dtype == "bf16" else "lmhead_f32_kernel",
+                     "kernel_us": lm_ms * 1e3, "algorithmic_bytes": nbytes,
+                     "algorithmic_flops": flops},
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the fp64 oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(case)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,203 @@
+/*
+ * eb.h - C ABI of the Early-Bird denoising-step library (libeb.so), MI355X / gfx950.
+ *
+ * One denoising step of a masked diffusion LM over ragged, variable-length active blocks
+ * (Early-Bird Decoding, Sec. 5 and Alg. 5):
+ *   1. bidirectional attention of each block's queries over the sequence's cached prefix
+ *      keys/values plus the block's own keys/values        -> eb_block_attn
+ *   2. LM-head logits z = W h for every block position, reduced on chip to the top-1
+ *      confidence kappa = max_v p(v), the top-1 token x_hat and the entropy of
+ *      p = softmax(z); the logits never reach device memory  -> eb_lmhead_confidence
+ *   3. threshold commit kappa >= tau with the anti-stall fallback inside each block
+ *                                                          -> eb_unmask_select
+ *   4. all of the above on one stream                      -> eb_decode_step
+ *
+ * Conventions shared by every entry point
+ *   - Every pointer argument is a DEVICE pointer owned by the caller unless stated
+ *     otherwise; descriptor structs themselves live in host memory and are read during the
+ *     call only.  The library allocates no device memory and keeps no state besides a
+ *     per-thread last-error string and cached device properties.
+ *   - Every call enqueues work on `stream` (a hipStream_t; NULL = default stream) and
+ *     returns without synchronising.  Outputs are valid once the stream reaches them.
+ *   - Arguments are checked on the host before anything is launched: a bad argument
+ *     returns EB_ERR_INVALID (or EB_ERR_WORKSPACE for a short workspace) and launches
+ *     nothing.  A valid but unimplemented combination returns EB_ERR_UNSUPPORTED.
+ *     A launch failure returns EB_ERR_HIP.  eb_last_error() describes the last failure
+ *     of the calling thread.
+ *   - Device-array contents are the caller's contract and are not checked: cu arrays are
+ *     non-decreasing, start at 0 and end at the totals given on the host, maxima are
+ *     true maxima, tau lies in (0, 1], inputs are finite.
+ *   - Rows are packed: the block rows of sequence b are rows cu_block[b] .. cu_block[b+1]-1,
+ *     in ascending sequence position (a non-contiguous block is gathered in order), its
+ *     cached prefix rows are cu_prefix[b] .. cu_prefix[b+1]-1.  Empty blocks are legal.
+ *   - bf16 tensors are raw bfloat16 bit patterns (uint16) and must be 16-byte aligned.
+ *   - Results are deterministic: the same inputs give bit-identical outputs run to run.
+ */
+#ifndef EB_H_
+#define EB_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* eb_stream_t; /* identical to hipStream_t */
+typedef struct ihipEvent_t* eb_event_t;   /* identical to hipEvent_t */
+
+typedef enum { EB_F32 = 0, EB_BF16 = 1 } eb_dtype;
+
+typedef enum {
+  EB_OK = 0,
+  EB_ERR_INVALID = 1,     /* bad argument; nothing launched */
+  EB_ERR_UNSUPPORTED = 2, /* valid but not implemented (e.g. head_dim not 64/128) */
+  EB_ERR_WORKSPACE = 3,   /* ws_bytes below the matching *_workspace() query */
+  EB_ERR_HIP = 4          /* HIP runtime / launch failure */
+} eb_status;
+
+/* Ragged batch.  Host integers size the launch grids; device arrays hold exclusive prefix
+ * sums of the per-sequence block and prefix lengths. */
+typedef struct {
+  int32_t batch;            /* number of sequences B >= 1 */
+  int32_t total_block;      /* T = cu_block[B] (block rows over all sequences) */
+  int32_t max_block;        /* max_b (cu_block[b+1] - cu_block[b]) */
+  int32_t total_prefix;     /* S = cu_prefix[B] (cached prefix rows) */
+  int32_t max_prefix;       /* max_b (cu_prefix[b+1] - cu_prefix[b]) */
+  const int32_t* cu_block;  /* device [B+1] */
+  const int32_t* cu_prefix; /* device [B+1]; unused (may be NULL) by eb_unmask_select */
+} eb_ragged;
+
+/* ---------------------------------------------------------------------------------------
+ * Block attention with a prefix KV cache (Sec. 3 / App. B: the mask predictor is a
+ * bidirectional Transformer, so a block query sees every key of its sequence; Sec. 6.3:
+ * keys/values of the committed context left of the block come from a prefix cache).
+ *
+ *   out[i, h, :] = sum_j softmax_j(scale * q[i, h, :] . k_j) v_j
+ *
+ * over the keys j of i's sequence b: its prefix rows (k_pre, v_pre) and its block rows
+ * (k_blk, v_blk).  No causal mask, no masking by [MASK] state.  Query head h reads key/value
+ * head h / (hq / hkv) (grouped-query attention with contiguous groups).  K arrives after any
+ * positional encoding.
+ *
+ *   q      [T, hq, head_dim]    k_blk, v_blk [T, hkv, head_dim]
+ *   k_pre, v_pre [S, hkv, head_dim]             out [T, hq, head_dim]   (all of dtype dt)
+ *
+ * Requires hq % hkv == 0, head_dim in {64, 128}, scale > 0 (pass 1/sqrt(head_dim)).
+ * Arithmetic: bf16 inputs, fp32 scores / softmax / accumulation, output rounded to bf16
+ * (round to nearest even); EB_F32 computes in fp32 throughout.
+ * ------------------------------------------------------------------------------------- */
+size_t eb_block_attn_workspace(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim);
+eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim,
+                        float scale, const void* q, const void* k_blk, const void* v_blk,
+                        const void* k_pre, const void* v_pre, void* out, void* ws,
+                        size_t ws_bytes, eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Fused LM head and confidence statistics (Alg. 5: softmax of the backbone logits, top-1
+ * confidence and token; Eq. app-confidence; Sec. 5.1: entropy, normalised by ln|V| for the
+ * block selector).  For each row i of h:
+ *
+ *   z = W h_i (fp32 accumulation),  p = softmax(z)
+ *   conf[i]         = max_v p(v)                      (kappa)
+ *   argmax[i]       = lowest v with z_v = max z       (x_hat; ties to the lowest id)
+ *   entropy_nats[i] = -sum_v p(v) ln p(v)             (raw nats; divide by ln(vocab) for H~)
+ *   max_logit[i]    = max_v z_v                       (optional; pass NULL to skip)
+ *
+ *   h [n_rows, hidden]   w [vocab, hidden] (nn.Linear layout)   outputs [n_rows]
+ *
+ * Requires n_rows >= 0, vocab >= 1, hidden >= 1; EB_BF16 also needs hidden % 64 == 0.
+ * ws: at least eb_lmhead_workspace(...) bytes of device memory, contents ignored; it holds
+ * per-(row, vocabulary slice) partial reductions merged in a fixed order.
+ * ------------------------------------------------------------------------------------- */
+size_t eb_lmhead_workspace(eb_dtype dt, int n_rows, int hidden, int vocab);
+eb_status eb_lmhead_confidence(eb_dtype dt, int n_rows, int hidden, int vocab, const void* h,
+                               const void* w, float* conf, float* entropy_nats,
+                               int32_t* argmax, float* max_logit, void* ws, size_t ws_bytes,
+                               eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Threshold unmask inside each variable-length block (Eq. prelim-update, threshold branch;
+ * Alg. 5 accept rule without the router term, anti-stall fallback and commit).
+ * For each sequence b, over its block rows i:
+ *
+ *   A_b = { i : masked[i] && conf[i] >= tau[b] }
+ *   if A_b is empty and some row is masked:
+ *       A_b = { the lowest i among masked rows with maximal conf[i] }
+ *   for i in A_b: tokens[i] = argmax[i]; masked[i] = 0
+ *   unmask[i]   = (i in A_b)            for every block row
+ *   n_commit[b] = |A_b|
+ *   resolved[b] = no masked row left in block b (1 for an empty block)
+ *
+ *   conf [T] f32, argmax [T] i32, tau [B] f32        (inputs)
+ *   masked [T] u8 (1 = [MASK]), tokens [T] i32         (updated in place)
+ *   unmask [T] u8, n_commit [B] i32, resolved [B] u8   (outputs)
+ *
+ * Only r->batch, r->total_block, r->max_block and r->cu_block are used.
+ * ------------------------------------------------------------------------------------- */
+eb_status eb_unmask_select(const eb_ragged* r, const float* conf, const int32_t* argmax,
+                           const float* tau, uint8_t* masked, int32_t* tokens, uint8_t* unmask,
+                           int32_t* n_commit, uint8_t* resolved, eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * One whole denoising step: eb_block_attn, then eb_lmhead_confidence over the T block rows
+ * of h, then eb_unmask_select, enqueued on one stream with no host synchronisation.
+ * Field meanings, layouts and requirements are those of the three calls above; the LM-head
+ * rows are the block rows (n_rows = ragged.total_block).
+ *
+ * Optional tracing: when `trace` is non-NULL, each non-NULL event in it is recorded on the
+ * step's stream at the named point (events created by the caller, e.g. with
+ * hipEventCreate); this times the kernels of one step without a host synchronisation.
+ * ------------------------------------------------------------------------------------- */
+typedef struct {
+  eb_event_t attn_begin, attn_end;     /* around the attention kernel */
+  eb_event_t lmhead_begin, lmhead_end; /* around the fused LM-head kernel (without its merge) */
+  eb_event_t select_begin, select_end; /* around the partial merge and the unmask kernels */
+} eb_step_trace;
+
+typedef struct {
+  eb_dtype dtype;
+  eb_ragged ragged;
+  /* attention */
+  int32_t hq, hkv, head_dim;
+  float attn_scale; /* <= 0 selects 1/sqrt(head_dim) */
+  const void* q;
+  const void* k_blk;
+  const void* v_blk;
+  const void* k_pre;
+  const void* v_pre;
+  void* attn_out;
+  /* LM head + statistics */
+  int32_t hidden, vocab;
+  const void* h;
+  const void* w;
+  float* conf;
+  float* entropy_nats;
+  int32_t* argmax;
+  float* max_logit; /* nullable */
+  /* unmask */
+  const float* tau;
+  uint8_t* masked;
+  int32_t* tokens;
+  uint8_t* unmask;
+  int32_t* n_commit;
+  uint8_t* resolved;
+  /* tracing */
+  const eb_step_trace* trace; /* nullable */
+} eb_step_desc;
+
+size_t eb_decode_step_workspace(const eb_step_desc* d);
+eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Diagnostics.
+ * ------------------------------------------------------------------------------------- */
+const char* eb_status_string(eb_status s); /* static string */
+const char* eb_last_error(void);           /* per-thread; "" if none; valid until next call */
+const char* eb_version(void);              /* static string */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EB_H_ */

@@ -1,0 +1,298 @@
+// Block attention with a prefix KV cache for gfx950.
+//
+// Every query row of a sequence's active block attends, without a causal mask, to the
+// sequence's cached prefix keys followed by the block's own keys.  Grouped-query attention:
+// query head h reads key/value head h / G with G = hq / hkv, so one workgroup serves the
+// G query heads of one key/value head and its K/V tiles are read once for all of them.
+//
+// bf16 path: scores are computed transposed, S^T = K Q^T, so each lane owns one query row
+// (an MFMA column) and reduces its softmax statistics in registers; the probabilities then
+// feed P V directly as the B operand of O^T = V^T P^T, with V staged transposed in LDS.
+#include "eb_common.hpp"
+#include "eb_internal.hpp"
+
+namespace eb {
+namespace {
+
+constexpr int kThreads = 256;   // 4 waves
+constexpr int kRowsPerWg = 128; // query rows (position, head-in-group) per workgroup
+constexpr int kKeys = 64;       // keys per LDS stage
+
+struct AttnParams {
+  const int32_t* cu_block;
+  const int32_t* cu_prefix;
+  int hq, hkv, group;
+  float scale_log2;  // scale * log2(e)
+  const uint16_t* q;
+  const uint16_t* k_blk;
+  const uint16_t* v_blk;
+  const uint16_t* k_pre;
+  const uint16_t* v_pre;
+  uint16_t* out;
+};
+
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16_bits_rne(lo)) |
+         (static_cast<uint32_t>(f32_to_bf16_bits_rne(hi)) << 16);
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
+  constexpr int kKRow = D + 8;       // K tile pitch (bf16)
+  constexpr int kVRow = kKeys + 4;   // V^T tile pitch (bf16)
+  constexpr int kDSteps = D / 16;    // MFMA k-steps over the head dimension
+  constexpr int kDBlocks = D / 32;   // 32-row blocks of O^T
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeys * kKRow];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * kVRow];
+
+  const int b = blockIdx.z;
+  const int g = blockIdx.y;
+  const int G = p.group;
+  const int bbeg = p.cu_block[b];
+  const int len = p.cu_block[b + 1] - bbeg;
+  const int pbeg = p.cu_prefix[b];
+  const int plen = p.cu_prefix[b + 1] - pbeg;
+  const int n_rows = len * G;
+  const int row0 = blockIdx.x * kRowsPerWg;
+  if (row0 >= n_rows) return;  // whole workgroup: this tile lies past the block
+  const int n_keys = plen + len;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+
+  // This lane's query row.
+  const int myrow = row0 + wave * 32 + l32;
+  const bool row_ok = myrow < n_rows;
+  const int rr = row_ok ? myrow : 0;
+  const int pos = rr / G, hh = rr % G;
+  const size_t q_off = (static_cast<size_t>(bbeg + pos) * p.hq + g * G + hh) * D;
+
+  // Q^T fragments (B operand): step s, half hf holds d = 16 s + 8 hf .. +7.
+  bf16x8 qf[kDSteps];
+#pragma unroll
+  for (int s = 0; s < kDSteps; ++s)
+    qf[s] = *reinterpret_cast<const bf16x8*>(p.q + q_off + 16 * s + 8 * half);
+
+  f32x16 o[kDBlocks];
+#pragma unroll
+  for (int db = 0; db < kDBlocks; ++db) o[db] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // Loader assignments.  K: 16-byte chunks, chunk c = key c / (D/8), columns 8 (c % (D/8)).
+  constexpr int kKChunks = kKeys * (D / 8);
+  constexpr int kKPer = kKChunks / kThreads;
+  // V: thread handles keys 2 kp, 2 kp + 1 (kp = tid % 32) and d range [dg * D/8, +D/8).
+  const int kp = tid & 31, dg = tid >> 5;
+  constexpr int kVd = D / 8;
+
+  auto key_src = [&](int j, const uint16_t* pre, const uint16_t* blk) -> const uint16_t* {
+    if (j < plen) return pre + (static_cast<size_t>(pbeg + j) * p.hkv + g) * D;
+    return blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
+  };
+
+  u32x4 kreg[kKPer];
+  u32x4 vreg[2][kVd / 8];
+  auto gload = [&](int kv0) {
+#pragma unroll
+    for (int i = 0; i < kKPer; ++i) {
+      const int c = tid + i * kThreads;
+      const int key = c / (D / 8), col = (c % (D / 8)) * 8;
+      const int j = kv0 + key;
+      kreg[i] = (j < n_keys) ? *reinterpret_cast<const u32x4*>(key_src(j, p.k_pre, p.k_blk) + col)
+                             : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int j = kv0 + 2 * kp + e;
+#pragma unroll
+      for (int c = 0; c < kVd / 8; ++c)
+        vreg[e][c] = (j < n_keys)
+                         ? *reinterpret_cast<const u32x4*>(key_src(j, p.v_pre, p.v_blk) +
+                                                          dg * kVd + 8 * c)
+                         : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < kKPer; ++i) {
+      const int c = tid + i * kThreads;
+      const int key = c / (D / 8), col = (c % (D / 8)) * 8;
+      *reinterpret_cast<u32x4*>(Ks + key * kKRow + col) = kreg[i];
+    }
+#pragma unroll
+    for (int c = 0; c < kVd / 8; ++c)
+#pragma unroll
+      for (int w4 = 0; w4 < 4; ++w4)
+#pragma unroll
+        for (int hw = 0; hw < 2; ++hw) {
+          const int d = dg * kVd + 8 * c + 2 * w4 + hw;
+          const uint32_t lo = (vreg[0][c][w4] >> (16 * hw)) & 0xffffu;
+          const uint32_t hi = (vreg[1][c][w4] >> (16 * hw)) & 0xffffu;
+          *reinterpret_cast<uint32_t*>(Vt + d * kVRow + 2 * kp) = lo | (hi << 16);
+        }
+  };
+
+  const int n_stages = (n_keys + kKeys - 1) / kKeys;
+  gload(0);
+  for (int st = 0; st < n_stages; ++st) {
+    const int kv0 = st * kKeys;
+    __syncthreads();  // previous stage's LDS reads are done
+    sstore();
+    __syncthreads();
+    if (st + 1 < n_stages) gload(kv0 + kKeys);
+
+    // S^T for two 32-key blocks: acc[kb][r] = S[query l32][key kb*32 + 8(r/4) + 4 half + r%4]
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      sacc[kb] = f32x16{};
+#pragma unroll
+      for (int s = 0; s < kDSteps; ++s) {
+        const bf16x8 kf =
+            *reinterpret_cast<const bf16x8*>(Ks + (kb * 32 + l32) * kKRow + 16 * s + 8 * half);
+        sacc[kb] = mfma32(kf, qf[s], sacc[kb]);
+      }
+    }
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kv0 + kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const float x = (key < n_keys) ? sacc[kb][r] * p.scale_log2 : -INFINITY;
+        sacc[kb][r] = x;
+        mloc = fmaxf(mloc, x);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float m_new = fmaxf(m_run, mloc);
+    const float alpha = fast_exp2(m_run - m_new);
+    m_run = m_new;
+    float lsum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = fast_exp2(sacc[kb][r] - m_new);
+        sacc[kb][r] = e;
+        lsum += e;
+      }
+    l_run = l_run * alpha + lsum;
+#pragma unroll
+    for (int db = 0; db < kDBlocks; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+
+    // O^T += V^T P^T.  MFMA u of key block kb covers keys kb*32 + 16u + {4 half + 0..3,
+    // 8 + 4 half + 0..3}, which are exactly accumulator registers 8u .. 8u+7 of sacc[kb].
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        u32x4 pb;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pb[e] = pack2_bf16(sacc[kb][8 * u + 2 * e], sacc[kb][8 * u + 2 * e + 1]);
+        const bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
+        const int kbase = kb * 32 + 16 * u + 4 * half;
+#pragma unroll
+        for (int db = 0; db < kDBlocks; ++db) {
+          const uint16_t* vr = Vt + (db * 32 + l32) * kVRow;
+          const u32x2 lo = *reinterpret_cast<const u32x2*>(vr + kbase);
+          const u32x2 hi = *reinterpret_cast<const u32x2*>(vr + kbase + 8);
+          const u32x4 va{lo[0], lo[1], hi[0], hi[1]};
+          o[db] = mfma32(__builtin_bit_cast(bf16x8, va), pf, o[db]);
+        }
+      }
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (!row_ok) return;
+  const float inv = 1.0f / l_tot;
+  uint16_t* dst = p.out + q_off;
+#pragma unroll
+  for (int db = 0; db < kDBlocks; ++db)
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int d = db * 32 + 8 * q4 + 4 * half;
+      const u32x2 v{pack2_bf16(o[db][4 * q4 + 0] * inv, o[db][4 * q4 + 1] * inv),
+                    pack2_bf16(o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv)};
+      *reinterpret_cast<u32x2*>(dst + d) = v;
+    }
+}
+
+// fp32 path (small shapes): one wavefront per (block row, query head); lanes split the head
+// dimension; keys are visited one by one with an online softmax.
+struct AttnParamsF32 {
+  const int32_t* cu_block;
+  const int32_t* cu_prefix;
+  int hq, hkv, group, head_dim;
+  float scale;
+  const float* q;
+  const float* k_blk;
+  const float* v_blk;
+  const float* k_pre;
+  const float* v_pre;
+  float* out;
+};
+
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnParamsF32 p) {
+  const int b = blockIdx.z, h = blockIdx.y, i = blockIdx.x;
+  const int bbeg = p.cu_block[b];
+  const int len = p.cu_block[b + 1] - bbeg;
+  if (i >= len) return;
+  const int pbeg = p.cu_prefix[b];
+  const int plen = p.cu_prefix[b + 1] - pbeg;
+  const int D = p.head_dim;
+  const int g = h / p.group;
+  const int lane = threadIdx.x;
+  const float* qr = p.q + (static_cast<size_t>(bbeg + i) * p.hq + h) * D;
+  const float q0 = lane < D ? qr[lane] : 0.f;
+  const float q1 = lane + 64 < D ? qr[lane + 64] : 0.f;
+  float m = -INFINITY, l = 0.f, a0 = 0.f, a1 = 0.f;
+  for (int j = 0; j < plen + len; ++j) {
+    const float* kr = (j < plen) ? p.k_pre + (static_cast<size_t>(pbeg + j) * p.hkv + g) * D
+                                 : p.k_blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
+    const float* vr = (j < plen) ? p.v_pre + (static_cast<size_t>(pbeg + j) * p.hkv + g) * D
+                                 : p.v_blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
+    float dot = (lane < D ? q0 * kr[lane] : 0.f) + (lane + 64 < D ? q1 * kr[lane + 64] : 0.f);
+    for (int mask = 32; mask >= 1; mask >>= 1) dot += __shfl_xor(dot, mask);
+    const float sc = dot * p.scale;
+    const float mn = fmaxf(m, sc);
+    const float alpha = expf(m - mn);
+    const float e = expf(sc - mn);
+    l = l * alpha + e;
+    a0 = a0 * alpha + e * (lane < D ? vr[lane] : 0.f);
+    a1 = a1 * alpha + e * (lane + 64 < D ? vr[lane + 64] : 0.f);
+    m = mn;
+  }
+  float* dst = p.out + (static_cast<size_t>(bbeg + i) * p.hq + h) * D;
+  if (lane < D) dst[lane] = a0 / l;
+  if (lane + 64 < D) dst[lane + 64] = a1 / l;
+}
+
+}  // namespace
+
+hipError_t block_attn(bool bf16, const AttnArgs& a, hipStream_t s) {
+  if (a.total_block == 0 || a.max_block == 0) return hipSuccess;
+  const int group = a.hq / a.hkv;
+  if (!bf16) {
+    AttnParamsF32 p{a.cu_block, a.cu_prefix, a.hq, a.hkv, group, a.head_dim, a.scale,
+                    static_cast<const float*>(a.q), static_cast<const float*>(a.k_blk),
+                    static_cast<const float*>(a.v_blk), static_cast<const float*>(a.k_pre),
+                    static_cast<const float*>(a.v_pre), static_cast<float*>(a.out)};
+    hipLaunchKernelGGL(attn_f32_kernel, dim3(a.max_block, a.hq, a.batch), dim3(64), 0, s, p);
+    return hipGetLastError();
+  }
+  AttnParams p{a.cu_block, a.cu_prefix, a.hq, a.hkv, group, a.scale * kLog2e,
+               static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k_blk),
+               static_cast<const uint16_t*>(a.v_blk), static_cast<const uint16_t*>(a.k_pre),
+               static_cast<const uint16_t*>(a.v_pre), static_cast<uint16_t*>(a.out)};
+  const long rows = static_cast<long>(a.max_block) * group;
+  dim3 grid(static_cast<unsigned>((rows + kRowsPerWg - 1) / kRowsPerWg), a.hkv, a.batch);
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace eb

@@ -1,0 +1,235 @@
+// C ABI of libeb.so: argument checks, workspace sizing, error reporting, step composition.
+// The declarations and the contract of every entry point are in include/eb.h.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "../../include/eb.h"
+#include "eb_internal.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+eb_status fail(eb_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+eb_status fail(eb_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+eb_status ok() {
+  g_last_error.clear();
+  return EB_OK;
+}
+
+eb_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(EB_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr size_t kWsAlign = 256;
+size_t round_up(size_t n) { return (n + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+eb_status check_ragged(const eb_ragged* r, bool need_prefix) {
+  if (!r) return fail(EB_ERR_INVALID, "ragged descriptor is NULL");
+  if (r->batch < 1) return fail(EB_ERR_INVALID, "batch must be >= 1 (got %d)", r->batch);
+  if (r->total_block < 0 || r->max_block < 0 || r->max_block > r->total_block)
+    return fail(EB_ERR_INVALID, "bad block totals (total_block %d, max_block %d)",
+                r->total_block, r->max_block);
+  if (r->total_block > 0 && r->max_block == 0)
+    return fail(EB_ERR_INVALID, "max_block is 0 but total_block is %d", r->total_block);
+  if (!r->cu_block) return fail(EB_ERR_INVALID, "cu_block is NULL");
+  if (need_prefix) {
+    if (r->total_prefix < 0 || r->max_prefix < 0 || r->max_prefix > r->total_prefix)
+      return fail(EB_ERR_INVALID, "bad prefix totals (total_prefix %d, max_prefix %d)",
+                  r->total_prefix, r->max_prefix);
+    if (!r->cu_prefix) return fail(EB_ERR_INVALID, "cu_prefix is NULL");
+  }
+  return EB_OK;
+}
+
+eb_status check_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim, float scale,
+                     const void* q, const void* k_blk, const void* v_blk, const void* k_pre,
+                     const void* v_pre, const void* out) {
+  if (dt != EB_F32 && dt != EB_BF16) return fail(EB_ERR_INVALID, "unknown dtype %d", (int)dt);
+  eb_status st = check_ragged(r, true);
+  if (st != EB_OK) return st;
+  if (hq < 1 || hkv < 1 || hq % hkv)
+    return fail(EB_ERR_INVALID, "need hq, hkv >= 1 and hq %% hkv == 0 (hq %d, hkv %d)", hq, hkv);
+  if (head_dim < 1) return fail(EB_ERR_INVALID, "head_dim must be >= 1 (got %d)", head_dim);
+  if (!(scale > 0.f) || !isfinite(scale))
+    return fail(EB_ERR_INVALID, "scale must be finite and > 0");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(EB_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", head_dim);
+  if (r->total_block > 0 && (!q || !k_blk || !v_blk || !out))
+    return fail(EB_ERR_INVALID, "NULL q / k_blk / v_blk / out");
+  if (r->total_prefix > 0 && (!k_pre || !v_pre))
+    return fail(EB_ERR_INVALID, "NULL k_pre / v_pre with total_prefix > 0");
+  if (dt == EB_BF16) {
+    const void* ps[] = {q, k_blk, v_blk, k_pre, v_pre, out};
+    for (const void* p : ps)
+      if (p && !aligned16(p)) return fail(EB_ERR_INVALID, "bf16 tensors must be 16-byte aligned");
+  }
+  return EB_OK;
+}
+
+eb_status check_lmhead(eb_dtype dt, int n_rows, int hidden, int vocab, const void* h,
+                       const void* w, const void* conf, const void* entropy,
+                       const void* argmax) {
+  if (dt != EB_F32 && dt != EB_BF16) return fail(EB_ERR_INVALID, "unknown dtype %d", (int)dt);
+  if (n_rows < 0 || hidden < 1 || vocab < 1)
+    return fail(EB_ERR_INVALID, "need n_rows >= 0, hidden >= 1, vocab >= 1 (got %d, %d, %d)",
+                n_rows, hidden, vocab);
+  if (dt == EB_BF16 && hidden % 64)
+    return fail(EB_ERR_UNSUPPORTED, "bf16 LM head needs hidden %% 64 == 0 (got %d)", hidden);
+  if (n_rows > 0 && (!h || !w || !conf || !entropy || !argmax))
+    return fail(EB_ERR_INVALID, "NULL h / w / conf / entropy / argmax");
+  if (dt == EB_BF16 && n_rows > 0 && (!aligned16(h) || !aligned16(w)))
+    return fail(EB_ERR_INVALID, "bf16 tensors must be 16-byte aligned");
+  return EB_OK;
+}
+
+eb_status check_unmask(const eb_ragged* r, const void* conf, const void* argmax, const void* tau,
+                       const void* masked, const void* tokens, const void* unmask,
+                       const void* n_commit, const void* resolved) {
+  eb_status st = check_ragged(r, false);
+  if (st != EB_OK) return st;
+  if (!tau || !n_commit || !resolved) return fail(EB_ERR_INVALID, "NULL tau / n_commit / resolved");
+  if (r->total_block > 0 && (!conf || !argmax || !masked || !tokens || !unmask))
+    return fail(EB_ERR_INVALID, "NULL conf / argmax / masked / tokens / unmask");
+  return EB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* eb_status_string(eb_status s) {
+  switch (s) {
+    case EB_OK: return "EB_OK";
+    case EB_ERR_INVALID: return "EB_ERR_INVALID";
+    case EB_ERR_UNSUPPORTED: return "EB_ERR_UNSUPPORTED";
+    case EB_ERR_WORKSPACE: return "EB_ERR_WORKSPACE";
+    case EB_ERR_HIP: return "EB_ERR_HIP";
+  }
+  return "EB_ERR_UNKNOWN";
+}
+
+const char* eb_last_error(void) { return g_last_error.c_str(); }
+
+const char* eb_version(void) { return "libeb 0.1 (gfx950)"; }
+
+size_t eb_block_attn_workspace(eb_dtype, const eb_ragged*, int, int, int) { return 0; }
+
+eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim,
+                        float scale, const void* q, const void* k_blk, const void* v_blk,
+                        const void* k_pre, const void* v_pre, void* out, void* ws,
+                        size_t ws_bytes, eb_stream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  eb_status st = check_attn(dt, r, hq, hkv, head_dim, scale, q, k_blk, v_blk, k_pre, v_pre, out);
+  if (st != EB_OK) return st;
+  eb::AttnArgs a{r->batch, r->total_block, r->max_block, r->total_prefix, r->max_prefix,
+                 r->cu_block, r->cu_prefix, hq, hkv, head_dim, scale, q, k_blk, v_blk,
+                 k_pre, v_pre, out};
+  return hip_status(eb::block_attn(dt == EB_BF16, a, stream), "eb_block_attn launch");
+}
+
+size_t eb_lmhead_workspace(eb_dtype dt, int n_rows, int hidden, int vocab) {
+  (void)hidden;
+  if (n_rows <= 0 || vocab <= 0) return 0;
+  return round_up(eb::lmhead_ws_bytes(dt == EB_BF16, n_rows, vocab));
+}
+
+eb_status eb_lmhead_confidence(eb_dtype dt, int n_rows, int hidden, int vocab, const void* h,
+                               const void* w, float* conf, float* entropy_nats,
+                               int32_t* argmax, float* max_logit, void* ws, size_t ws_bytes,
+                               eb_stream_t stream) {
+  eb_status st = check_lmhead(dt, n_rows, hidden, vocab, h, w, conf, entropy_nats, argmax);
+  if (st != EB_OK) return st;
+  const size_t need = eb_lmhead_workspace(dt, n_rows, hidden, vocab);
+  if (ws_bytes < need || (need && !ws))
+    return fail(EB_ERR_WORKSPACE, "LM-head workspace %zu bytes < required %zu", ws_bytes, need);
+  if (n_rows == 0) return ok();
+  const bool bf16 = dt == EB_BF16;
+  hipError_t e = eb::lmhead_partials(bf16, n_rows, hidden, vocab, h, w, ws, stream);
+  if (e != hipSuccess) return hip_status(e, "LM-head partial launch");
+  e = eb::lmhead_combine(n_rows, eb::lmhead_num_slices(bf16, n_rows, vocab), ws, conf,
+                         entropy_nats, argmax, max_logit, stream);
+  return hip_status(e, "LM-head combine launch");
+}
+
+eb_status eb_unmask_select(const eb_ragged* r, const float* conf, const int32_t* argmax,
+                           const float* tau, uint8_t* masked, int32_t* tokens, uint8_t* unmask,
+                           int32_t* n_commit, uint8_t* resolved, eb_stream_t stream) {
+  eb_status st = check_unmask(r, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved);
+  if (st != EB_OK) return st;
+  return hip_status(eb::unmask_select(r->batch, r->max_block, r->cu_block, conf, argmax, tau,
+                                      masked, tokens, unmask, n_commit, resolved, stream),
+                    "eb_unmask_select launch");
+}
+
+size_t eb_decode_step_workspace(const eb_step_desc* d) {
+  if (!d) return 0;
+  return round_up(eb_block_attn_workspace(d->dtype, &d->ragged, d->hq, d->hkv, d->head_dim)) +
+         eb_lmhead_workspace(d->dtype, d->ragged.total_block, d->hidden, d->vocab);
+}
+
+eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_stream_t stream) {
+  if (!d) return fail(EB_ERR_INVALID, "step descriptor is NULL");
+  const float scale = d->attn_scale > 0.f ? d->attn_scale : 1.0f / sqrtf((float)d->head_dim);
+  eb_status st = check_attn(d->dtype, &d->ragged, d->hq, d->hkv, d->head_dim, scale, d->q,
+                            d->k_blk, d->v_blk, d->k_pre, d->v_pre, d->attn_out);
+  if (st != EB_OK) return st;
+  const int T = d->ragged.total_block;
+  st = check_lmhead(d->dtype, T, d->hidden, d->vocab, d->h, d->w, d->conf, d->entropy_nats,
+                    d->argmax);
+  if (st != EB_OK) return st;
+  st = check_unmask(&d->ragged, d->conf, d->argmax, d->tau, d->masked, d->tokens, d->unmask,
+                    d->n_commit, d->resolved);
+  if (st != EB_OK) return st;
+  const size_t need = eb_decode_step_workspace(d);
+  if (ws_bytes < need || (need && !ws))
+    return fail(EB_ERR_WORKSPACE, "step workspace %zu bytes < required %zu", ws_bytes, need);
+
+  const bool bf16 = d->dtype == EB_BF16;
+  const eb_ragged* r = &d->ragged;
+  const eb_step_trace* tr = d->trace;
+  auto mark = [&](eb_event_t ev) -> hipError_t {
+    return ev ? hipEventRecord(reinterpret_cast<hipEvent_t>(ev), stream) : hipSuccess;
+  };
+  eb::AttnArgs a{r->batch, r->total_block, r->max_block, r->total_prefix, r->max_prefix,
+                 r->cu_block, r->cu_prefix, d->hq, d->hkv, d->head_dim, scale, d->q, d->k_blk,
+                 d->v_blk, d->k_pre, d->v_pre, d->attn_out};
+  hipError_t e = tr ? mark(tr->attn_begin) : hipSuccess;
+  if (e == hipSuccess) e = eb::block_attn(bf16, a, stream);
+  if (e == hipSuccess && tr) e = mark(tr->attn_end);
+  if (e != hipSuccess) return hip_status(e, "step attention launch");
+  char* lm_ws = static_cast<char*>(ws) +
+                round_up(eb_block_attn_workspace(d->dtype, r, d->hq, d->hkv, d->head_dim));
+  if (tr) e = mark(tr->lmhead_begin);
+  if (e == hipSuccess && T > 0)
+    e = eb::lmhead_partials(bf16, T, d->hidden, d->vocab, d->h, d->w, lm_ws, stream);
+  if (e == hipSuccess && tr) e = mark(tr->lmhead_end);
+  if (e != hipSuccess) return hip_status(e, "step LM-head launch");
+  if (tr) e = mark(tr->select_begin);
+  if (e == hipSuccess && T > 0)
+    e = eb::lmhead_combine(T, eb::lmhead_num_slices(bf16, T, d->vocab), lm_ws, d->conf,
+                           d->entropy_nats, d->argmax, d->max_logit, stream);
+  if (e == hipSuccess)
+    e = eb::unmask_select(r->batch, r->max_block, r->cu_block, d->conf, d->argmax, d->tau,
+                          d->masked, d->tokens, d->unmask, d->n_commit, d->resolved, stream);
+  if (e == hipSuccess && tr) e = mark(tr->select_end);
+  return hip_status(e, "step select launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,86 @@
+// Device-side helpers shared by the gfx950 kernels: bf16 vectors, MFMA wrappers, and the
+// (max, sum, entropy-moment, argmax) partial used to reduce softmax statistics over a
+// vocabulary that never leaves the chip.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace eb {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kNegBig = -3.402823466e38f;  // empty-partial max (finite, so 0 * (m - M) = 0)
+constexpr int32_t kNoIndex = 0x7fffffff;
+
+// 32x32 output tile, K = 16 per instruction, bf16 inputs, fp32 accumulate.
+// Lane l holds A[l % 32][8 * (l / 32) + 0..7] and B[8 * (l / 32) + 0..7][l % 32];
+// accumulator register r of lane l is C[8 * (r / 4) + 4 * (l / 32) + r % 4][l % 32].
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// bf16 <-> f32
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t u) {
+  return __uint_as_float(static_cast<uint32_t>(u) << 16);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16_bits_rne(float f) {
+  uint32_t b = __float_as_uint(f);
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return static_cast<uint16_t>(b >> 16);
+}
+
+// Partial softmax statistics of a set of logits, in base-2 units:
+//   m = max z,  s = sum 2^((z - m) log2 e),  t = sum 2^((z - m) log2 e) * (z - m) log2 e,
+//   idx = lowest index attaining m.
+// Then kappa = 1 / s and H = ln s - ln2 * t / s.
+struct Partial {
+  float m, s, t;
+  int32_t idx;
+};
+
+__device__ __forceinline__ Partial partial_empty() { return Partial{kNegBig, 0.f, 0.f, kNoIndex}; }
+
+// Merge two partials.  The result does not depend on argument order for m and idx; s and t
+// are combined in the order given (callers fix that order for determinism).
+__device__ __forceinline__ Partial partial_merge(const Partial& a, const Partial& b) {
+  const float M = fmaxf(a.m, b.m);
+  // <= 0; clamped so that an empty side (s = 0, m = kNegBig) contributes 0 * finite = 0
+  const float da = fmaxf((a.m - M) * kLog2e, -1.0e30f);
+  const float db = fmaxf((b.m - M) * kLog2e, -1.0e30f);
+  const float fa = fast_exp2(da);
+  const float fb = fast_exp2(db);
+  Partial r;
+  r.m = M;
+  r.s = a.s * fa + b.s * fb;
+  r.t = fa * (a.t + a.s * da) + fb * (b.t + b.s * db);
+  r.idx = (a.m > b.m) ? a.idx : (b.m > a.m) ? b.idx : min(a.idx, b.idx);
+  return r;
+}
+
+__device__ __forceinline__ Partial partial_shfl_xor(const Partial& p, int mask) {
+  Partial q;
+  q.m = __shfl_xor(p.m, mask);
+  q.s = __shfl_xor(p.s, mask);
+  q.t = __shfl_xor(p.t, mask);
+  q.idx = __shfl_xor(p.idx, mask);
+  return q;
+}
+
+// Butterfly step: lanes lane and lane ^ mask both end with merge(lower lane, higher lane),
+// evaluated by the same expression, hence bit-identical on both lanes.
+__device__ __forceinline__ Partial partial_xor_merge(const Partial& p, int mask, int lane) {
+  const Partial q = partial_shfl_xor(p, mask);
+  return (lane & mask) ? partial_merge(q, p) : partial_merge(p, q);
+}
+
+}  // namespace eb

@@ -1,0 +1,39 @@
+// Host-side launch interface between the C ABI (eb_api.hip) and the kernel files.
+// Callers have validated every argument; these functions only choose tiles and launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace eb {
+
+// ---- LM head + confidence -------------------------------------------------------------
+// Number of vocabulary slices whose per-row partials are written to the workspace.
+int lmhead_num_slices(bool bf16, int n_rows, int vocab);
+size_t lmhead_ws_bytes(bool bf16, int n_rows, int vocab);
+// Partials [n_rows, n_slices] go to ws; the combine writes the per-row outputs.
+hipError_t lmhead_partials(bool bf16, int n_rows, int hidden, int vocab, const void* h,
+                           const void* w, void* ws, hipStream_t s);
+hipError_t lmhead_combine(int n_rows, int n_slices, const void* ws, float* conf,
+                          float* entropy, int32_t* argmax, float* max_logit, hipStream_t s);
+
+// ---- block attention ------------------------------------------------------------------
+struct AttnArgs {
+  int batch, total_block, max_block, total_prefix, max_prefix;
+  const int32_t* cu_block;
+  const int32_t* cu_prefix;
+  int hq, hkv, head_dim;
+  float scale;
+  const void *q, *k_blk, *v_blk, *k_pre, *v_pre;
+  void* out;
+};
+hipError_t block_attn(bool bf16, const AttnArgs& a, hipStream_t s);
+
+// ---- unmask ---------------------------------------------------------------------------
+hipError_t unmask_select(int batch, int max_block, const int32_t* cu_block, const float* conf,
+                         const int32_t* argmax, const float* tau, uint8_t* masked,
+                         int32_t* tokens, uint8_t* unmask, int32_t* n_commit, uint8_t* resolved,
+                         hipStream_t s);
+
+}  // namespace eb

@@ -1,0 +1,85 @@
+"""The C ABI library loads, exports every function include/eb.h declares, and rejects bad
+arguments on the host (no GPU work is launched by any of these calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_16450_amd import binding as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "eb.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(eb_[a-z0-9_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_header_declares_the_step_entry_points():
+    names = declared_functions()
+    for n in ("eb_block_attn", "eb_lmhead_confidence", "eb_unmask_select", "eb_decode_step"):
+        assert n in names
+
+
+def test_library_exports_every_declared_function():
+    lib = B.load()
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+    assert set(declared_functions()) == set(B.EXPORTS)
+
+
+def _ragged(batch=1, T=4, maxb=4, S=0, maxp=0, cu_b=0x1000, cu_p=0x2000):
+    return B.eb_ragged(batch, T, maxb, S, maxp, cu_b, cu_p)
+
+
+def test_invalid_arguments_are_rejected_before_launch():
+    lib = B.load()
+    r = _ragged(batch=0)
+    assert lib.eb_unmask_select(ctypes.byref(r), *([None] * 9)) == B.EB_ERR_INVALID
+    assert "batch" in B.eb_last_error()
+    r = _ragged()
+    # NULL outputs
+    assert lib.eb_unmask_select(ctypes.byref(r), *([None] * 9)) == B.EB_ERR_INVALID
+    # hq not a multiple of hkv
+    assert lib.eb_block_attn(B.EB_BF16, ctypes.byref(r), 6, 4, 128, 0.1, *([0x100] * 6), None, 0,
+                             None) == B.EB_ERR_INVALID
+    # head_dim 96 is valid but unimplemented
+    assert lib.eb_block_attn(B.EB_BF16, ctypes.byref(r), 4, 4, 96, 0.1, *([0x100] * 6), None, 0,
+                             None) == B.EB_ERR_UNSUPPORTED
+    # misaligned bf16 pointer
+    assert lib.eb_block_attn(B.EB_BF16, ctypes.byref(r), 4, 4, 128, 0.1, 0x101, *([0x100] * 5),
+                             None, 0, None) == B.EB_ERR_INVALID
+    # non-positive scale
+    assert lib.eb_block_attn(B.EB_BF16, ctypes.byref(r), 4, 4, 128, 0.0, *([0x100] * 6), None, 0,
+                             None) == B.EB_ERR_INVALID
+    # unknown dtype
+    assert lib.eb_lmhead_confidence(7, 4, 64, 100, *([0x100] * 5), None, None, 0, None) == \
+        B.EB_ERR_INVALID
+    # bf16 hidden not a multiple of 64
+    assert lib.eb_lmhead_confidence(B.EB_BF16, 4, 96, 100, *([0x100] * 5), None, None, 0, None) \
+        == B.EB_ERR_UNSUPPORTED
+    # short workspace
+    need = lib.eb_lmhead_workspace(B.EB_BF16, 4, 64, 1000)
+    assert need > 0
+    assert lib.eb_lmhead_confidence(B.EB_BF16, 4, 64, 1000, *([0x100] * 5), None, 0x100, need - 1,
+                                    None) == B.EB_ERR_WORKSPACE
+    assert "workspace" in B.eb_last_error()
+
+
+def test_workspace_queries():
+    lib = B.load()
+    assert lib.eb_lmhead_workspace(B.EB_BF16, 0, 4096, 126464) == 0
+    small = lib.eb_lmhead_workspace(B.EB_BF16, 32, 4096, 126464)
+    big = lib.eb_lmhead_workspace(B.EB_BF16, 64, 4096, 126464)
+    assert small > 0 and big >= 2 * small - 256 and small % 256 == 0
+    r = _ragged()
+    assert lib.eb_block_attn_workspace(B.EB_BF16, ctypes.byref(r), 4, 4, 128) == 0
+
+
+def test_status_strings():
+    assert B.eb_status_string(0) == "EB_OK"
+    assert B.eb_status_string(3) == "EB_ERR_WORKSPACE"
+    assert "gfx950" in B.eb_version()

@@ -1,0 +1,291 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Bars (written here, enforced below):
+  * argmax token ids, unmask flags, committed tokens, mask flags, n_commit, resolved:
+    bit-exact (inputs carry away-from-tie margins, see oracle/margins.py);
+  * kappa and raw entropy (nats): within 1e-3 absolute;
+  * max logit within ARGMAX_GAP / 4 and ln kappa within 1e-3 (the margins suffice);
+  * attention output: bf16 within rtol 2e-2 / atol 2e-2, fp32 within 1e-4.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import margins
+from paper_2609_16450_amd import (EB_BF16, Ragged, eb_block_attn, eb_decode_step,
+                                  eb_lmhead_confidence, eb_unmask_select)
+from paper_2609_16450_amd.device_case import DeviceStep
+from tests._cases import as_f32, enforce_margins
+from workloads import CONFIGS, custom_config, make_step
+
+pytestmark = pytest.mark.gpu
+
+ATTN_TOL_BF16 = dict(rtol=2e-2, atol=2e-2)
+ATTN_TOL_F32 = dict(rtol=1e-4, atol=1e-4)
+STAT_ATOL = 1e-3
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def attn_out_f32(t: torch.Tensor) -> np.ndarray:
+    return t.float().cpu().numpy()
+
+
+def check_stats(gpu_conf, gpu_ent, gpu_arg, gpu_ml, ref, rows=None):
+    sel = slice(None) if rows is None else rows
+    np.testing.assert_array_equal(gpu_arg[sel], ref["argmax"])
+    np.testing.assert_allclose(gpu_conf[sel], ref["conf"], rtol=0, atol=STAT_ATOL)
+    np.testing.assert_allclose(gpu_ent[sel], ref["entropy"], rtol=0, atol=STAT_ATOL)
+    assert np.max(np.abs(gpu_ml[sel] - ref["max_logit"])) < margins.ARGMAX_GAP / 4
+    assert np.max(np.abs(np.log(gpu_conf[sel]) - np.log(ref["conf"]))) < 1e-3
+
+
+# ----------------------------------------------------------------------------------------
+# LM head + statistics, small shapes spanning several tiles and ragged tails
+# ----------------------------------------------------------------------------------------
+LM_CASES = [
+    # (n_rows, hidden, vocab, dtype)
+    (1, 64, 1000, "bf16"),
+    (5, 256, 2048 + 77, "bf16"),
+    (32, 320, 3000, "bf16"),
+    (33, 128, 1537, "bf16"),
+    (64, 192, 4099, "bf16"),
+    (65, 256, 2500, "bf16"),
+    (200, 512, 5000, "bf16"),
+    (32, 256, 2048, "f32"),
+    (7, 100, 999, "f32"),
+]
+
+
+@pytest.mark.parametrize("n_rows,hidden,vocab,dt", LM_CASES)
+def test_lmhead_small(n_rows, hidden, vocab, dt):
+    say(f"lmhead n_rows={n_rows} hidden={hidden} vocab={vocab} dtype={dt}")
+    cfg = custom_config(seed=11 + n_rows, block_len=("fixed", n_rows), hidden=hidden, vocab=vocab,
+                        dtype=dt, hq=1, hkv=1, head_dim=64, prefix_len=("fixed", 0))
+    case = enforce_margins(make_step(cfg))
+    ref = oracle.lmhead_confidence(as_f32(case.h, dt), as_f32(case.w, dt))
+    ds = DeviceStep(case)
+    eb_lmhead_confidence(ds.h, ds.w, ds.conf, ds.entropy, ds.argmax, ds.max_logit)
+    torch.cuda.synchronize()
+    check_stats(ds.conf.cpu().numpy(), ds.entropy.cpu().numpy(), ds.argmax.cpu().numpy(),
+                ds.max_logit.cpu().numpy(), ref)
+
+
+def test_lmhead_vocab_ties_take_lowest_id():
+    # Duplicate rows of W give bit-identical logits (same accumulation order, no split over the
+    # hidden dimension), so the lowest duplicated id must win.
+    say("lmhead ties")
+    rng = np.random.default_rng(5)
+    n, d, V = 40, 256, 3000
+    h = torch.from_numpy(rng.standard_normal((n, d)).astype(np.float32)).to(torch.bfloat16).cuda()
+    w = torch.from_numpy((rng.standard_normal((V, d)) / 16).astype(np.float32)).to(torch.bfloat16)
+    # make row 2900 the clear winner for every position, then copy it to ids 130 and 2999
+    w[2900] = (h.float().cpu().mean(0) * 4).to(torch.bfloat16)
+    w[130] = w[2900]
+    w[2999] = w[2900]
+    w = w.cuda()
+    conf = torch.empty(n, device="cuda")
+    ent = torch.empty(n, device="cuda")
+    am = torch.empty(n, dtype=torch.int32, device="cuda")
+    eb_lmhead_confidence(h, w, conf, ent, am)
+    torch.cuda.synchronize()
+    z = h.float().cpu().double().numpy() @ w.float().cpu().double().numpy().T
+    m = z.max(1)
+    winners = [np.flatnonzero(z[i] == m[i])[0] for i in range(n)]
+    np.testing.assert_array_equal(am.cpu().numpy(), winners)
+    assert (am.cpu().numpy() == 130).sum() > 0
+
+
+# ----------------------------------------------------------------------------------------
+# block attention, small ragged shapes
+# ----------------------------------------------------------------------------------------
+ATTN_CASES = [
+    # batch, hq, hkv, D, block_len spec, prefix_len spec, dtype
+    (1, 4, 4, 64, ("fixed", 32), ("fixed", 96), "f32"),
+    (3, 4, 2, 64, ("uniform", 0, 20), ("uniform", 0, 70), "f32"),
+    (1, 2, 2, 128, ("fixed", 1), ("fixed", 0), "bf16"),
+    (4, 8, 2, 128, ("uniform", 0, 40), ("uniform", 0, 200), "bf16"),
+    (3, 6, 6, 64, ("uniform", 1, 70), ("uniform", 60, 130), "bf16"),
+    (2, 28, 4, 128, ("uniform", 10, 60), ("fixed", 300), "bf16"),
+    (5, 4, 1, 128, ("choice", (0, 1, 63, 64, 65, 129)), ("choice", (0, 1, 63, 64, 65)), "bf16"),
+]
+
+
+@pytest.mark.parametrize("batch,hq,hkv,D,bl,pl,dt", ATTN_CASES)
+def test_block_attn_small(batch, hq, hkv, D, bl, pl, dt):
+    say(f"attn batch={batch} hq={hq} hkv={hkv} D={D} bl={bl} pl={pl} dtype={dt}")
+    cfg = custom_config(seed=100 + batch * hq, batch=batch, hq=hq, hkv=hkv, head_dim=D,
+                        block_len=bl, prefix_len=pl, hidden=64, vocab=64, dtype=dt)
+    case = make_step(cfg)
+    if case.T == 0:
+        pytest.skip("all blocks empty")
+    f = {k: as_f32(getattr(case, k), dt) for k in ("q", "k_blk", "v_blk", "k_pre", "v_pre")}
+    ref = oracle.block_attention(**f, cu_block=case.cu_block, cu_prefix=case.cu_prefix,
+                                 hq=hq, hkv=hkv)
+    ds = DeviceStep(case)
+    eb_block_attn(ds.ragged, ds.q, ds.k_blk, ds.v_blk, ds.k_pre, ds.v_pre, ds.attn_out)
+    torch.cuda.synchronize()
+    tol = ATTN_TOL_BF16 if dt == "bf16" else ATTN_TOL_F32
+    np.testing.assert_allclose(attn_out_f32(ds.attn_out), ref, **tol)
+
+
+# ----------------------------------------------------------------------------------------
+# unmask: constructed confidences (exact ties, kappa == tau, empty and length-1 blocks)
+# ----------------------------------------------------------------------------------------
+def _run_unmask(lens, conf, masked, argmax, tokens, tau):
+    r = Ragged.from_lengths(lens, [0] * len(lens))
+    T, B = r.total_block, r.batch
+    d = lambda x, dt: torch.from_numpy(np.asarray(x, dtype=dt)).cuda()
+    c, a, t = d(conf, np.float32), d(argmax, np.int32), d(tau, np.float32)
+    m, tk = d(masked, np.uint8), d(tokens, np.int32)
+    un = torch.full((T,), 7, dtype=torch.uint8, device="cuda")
+    nc = torch.full((B,), -5, dtype=torch.int32, device="cuda")
+    rs = torch.full((B,), 9, dtype=torch.uint8, device="cuda")
+    eb_unmask_select(r, c, a, t, m, tk, un, nc, rs)
+    torch.cuda.synchronize()
+    return dict(unmask=un.cpu().numpy(), tokens=tk.cpu().numpy(), masked=m.cpu().numpy(),
+                n_commit=nc.cpu().numpy(), resolved=rs.cpu().numpy())
+
+
+def _compare_unmask(lens, conf, masked, argmax, tokens, tau):
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    ref = oracle.unmask_select(conf, argmax, masked, tokens, tau, cu)
+    got = _run_unmask(lens, conf, masked, argmax, tokens, tau)
+    for k in ("unmask", "tokens", "masked", "n_commit", "resolved"):
+        np.testing.assert_array_equal(got[k], ref[k], err_msg=k)
+
+
+def test_unmask_constructed_edge_cases():
+    say("unmask edge cases")
+    rng = np.random.default_rng(0)
+    levels = np.array([0.1, 0.5, 0.9, 0.95, 1.0], np.float32)
+    lens = [0, 1, 1, 2, 5, 6, 0, 33, 256, 257, 700, 3]
+    T = sum(lens)
+    conf = levels[rng.integers(0, levels.size, T)]
+    masked = (rng.random(T) < 0.6).astype(np.uint8)
+    # block 1: single masked row below tau; block 2: single unmasked row
+    conf[0], masked[0] = 0.1, 1
+    masked[1] = 0
+    # block 3: two masked rows with equal conf below tau -> lower wins
+    conf[2:4], masked[2:4] = 0.5, 1
+    # block 4: every row masked and exactly at tau
+    conf[4:9], masked[4:9] = 0.9, 1
+    argmax = rng.integers(0, 1000, T).astype(np.int32)
+    tokens = np.where(masked == 1, -1, rng.integers(0, 1000, T)).astype(np.int32)
+    tau = np.full(len(lens), 0.9, np.float32)
+    tau[5] = 1.0
+    _compare_unmask(lens, conf, masked, argmax, tokens, tau)
+
+
+def test_unmask_random_ragged_with_ties():
+    say("unmask random")
+    rng = np.random.default_rng(1)
+    for it in range(20):
+        B = int(rng.integers(1, 70))
+        lens = rng.integers(0, 300, B).tolist()
+        T = sum(lens)
+        # coarse grid of confidences gives many exact ties
+        conf = (rng.integers(0, 20, T) / 20.0).astype(np.float32)
+        masked = (rng.random(T) < rng.random()).astype(np.uint8)
+        argmax = rng.integers(0, 152064, T).astype(np.int32)
+        tokens = np.where(masked == 1, -1, rng.integers(0, 152064, T)).astype(np.int32)
+        tau = rng.choice(np.array([0.7, 0.8, 0.9, 0.95], np.float32), B)
+        _compare_unmask(lens, conf, masked, argmax, tokens, tau)
+
+
+# ----------------------------------------------------------------------------------------
+# whole step on the named workloads, in the launch configuration the benchmark times
+# ----------------------------------------------------------------------------------------
+def _sample_blocks(case, k=3):
+    lens = case.block_lens
+    nonempty = np.flatnonzero(lens > 0)
+    if nonempty.size <= k:
+        return nonempty.tolist()
+    rng = np.random.default_rng(case.cfg.seed + 77)
+    pick = {int(nonempty[0]), int(nonempty[np.argmax(lens[nonempty])])}
+    while len(pick) < k:
+        pick.add(int(rng.choice(nonempty)))
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_decode_step_workload(name):
+    say(f"decode_step workload={name}")
+    case = make_step(name)
+    full = case.T <= 64
+    blocks = list(range(case.batch)) if full else _sample_blocks(case)
+    enforce_margins(case, blocks)
+    dt = case.dtype
+    ds = DeviceStep(case)
+    eb_decode_step(ds.buffers)
+    torch.cuda.synchronize()
+    say(f"  gpu done; oracle over blocks {blocks}")
+
+    rows = np.concatenate([np.arange(case.cu_block[b], case.cu_block[b + 1]) for b in blocks])
+    conf = ds.conf.cpu().numpy()
+    ent = ds.entropy.cpu().numpy()
+    am = ds.argmax.cpu().numpy()
+    ml = ds.max_logit.cpu().numpy()
+    ref = oracle.lmhead_confidence(as_f32(case.h, dt), as_f32(case.w, dt), rows=rows)
+    check_stats(conf, ent, am, ml, ref, rows)
+
+    # unmask on the checked blocks, from the oracle's own statistics
+    sub_lens = [int(case.block_lens[b]) for b in blocks]
+    sub_cu = np.concatenate([[0], np.cumsum(sub_lens)]).astype(np.int32)
+    uref = oracle.unmask_select(ref["conf"], ref["argmax"], case.masked[rows], case.tokens[rows],
+                                case.tau[blocks], sub_cu)
+    np.testing.assert_array_equal(ds.unmask.cpu().numpy()[rows], uref["unmask"])
+    np.testing.assert_array_equal(ds.tokens.cpu().numpy()[rows], uref["tokens"])
+    np.testing.assert_array_equal(ds.masked.cpu().numpy()[rows], uref["masked"])
+    np.testing.assert_array_equal(ds.n_commit.cpu().numpy()[blocks], uref["n_commit"])
+    np.testing.assert_array_equal(ds.resolved.cpu().numpy()[blocks], uref["resolved"])
+
+    # attention on the checked sequences
+    sub_pl = [int(case.prefix_lens[b]) for b in blocks]
+    prow = np.concatenate([np.arange(case.cu_prefix[b], case.cu_prefix[b + 1]) for b in blocks])
+    f = lambda a: as_f32(a, dt)
+    aref = oracle.block_attention(f(case.q[rows]), f(case.k_blk[rows]), f(case.v_blk[rows]),
+                                  f(case.k_pre[prow]), f(case.v_pre[prow]), sub_cu,
+                                  np.concatenate([[0], np.cumsum(sub_pl)]).astype(np.int32),
+                                  case.cfg.hq, case.cfg.hkv)
+    tol = ATTN_TOL_BF16 if dt == "bf16" else ATTN_TOL_F32
+    np.testing.assert_allclose(attn_out_f32(ds.attn_out)[rows], aref, **tol)
+
+    # properties over every row and block
+    V = case.cfg.vocab
+    assert (am >= 0).all() and (am < V).all()
+    assert (conf > 0).all() and (conf <= 1.0 + 1e-6).all()
+    assert (ent >= -1e-4).all() and (ent <= math.log(V) + 1e-3).all()
+    assert (ent >= -np.log(conf) - 1e-3).all()
+    un = ds.unmask.cpu().numpy().astype(bool)
+    m0 = case.masked.astype(bool)
+    assert not (un & ~m0).any()
+    np.testing.assert_array_equal(ds.tokens.cpu().numpy()[un], am[un])
+    nc = ds.n_commit.cpu().numpy()
+    for b in range(case.batch):
+        sl = slice(case.cu_block[b], case.cu_block[b + 1])
+        assert nc[b] == un[sl].sum()
+        assert (nc[b] >= 1) == m0[sl].any()
+
+
+def test_decode_step_is_deterministic():
+    say("determinism llada8b_b16")
+    case = make_step("llada8b_b16")
+    ds = DeviceStep(case)
+    outs = []
+    for _ in range(2):
+        ds.reset_state()
+        eb_decode_step(ds.buffers)
+        torch.cuda.synchronize()
+        outs.append([t.clone() for t in (ds.attn_out, ds.conf, ds.entropy, ds.argmax, ds.max_logit,
+                                         ds.tokens, ds.masked, ds.unmask, ds.n_commit, ds.resolved)])
+    for a, b in zip(*outs):
+        assert torch.equal(a.view(torch.uint8) if a.dtype == torch.bfloat16 else a,
+                           b.view(torch.uint8) if b.dtype == torch.bfloat16 else b)
