@@ -157,15 +157,15 @@ __global__ __launch_bounds__(C::kThreads) void lmhead_bf16_kernel(
           idx = v;
         }
       }
+    // y = (z - m) log2 e is exactly 0 at the maximum, so s >= 1 and kappa = 1/s <= 1.
     float s = 0.f, t = 0.f;
-    const float mb = m * kLog2e;
 #pragma unroll
     for (int tm = 0; tm < C::TM; ++tm)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int v = v0 + wm * C::kWaveM + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
         if (v < vocab) {
-          const float y = fmaf(acc[tm][tn][r], kLog2e, -mb);
+          const float y = (acc[tm][tn][r] - m) * kLog2e;
           const float e = fast_exp2(y);
           s += e;
           t = fmaf(e, y, t);

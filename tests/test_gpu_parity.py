@@ -261,7 +261,7 @@ def test_decode_step_workload(name):
     # properties over every row and block
     V = case.cfg.vocab
     assert (am >= 0).all() and (am < V).all()
-    assert (conf > 0).all() and (conf <= 1.0 + 1e-6).all()
+    assert (conf > 0).all() and (conf <= 1.0).all()
     assert (ent >= -1e-4).all() and (ent <= math.log(V) + 1e-3).all()
     assert (ent >= -np.log(conf) - 1e-3).all()
     un = ds.unmask.cpu().numpy().astype(bool)
