@@ -90,6 +90,8 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
     return blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
   };
 
+  // Loads are unconditional with clamped key indices (a conditional load would be waited for
+  // on the spot); keys past the end are replaced by zeros when stored to LDS.
   u32x4 kreg[kKPer];
   u32x4 vreg[2][kVd / 8];
   auto gload = [&](int kv0) {
@@ -97,28 +99,26 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
     for (int i = 0; i < kKPer; ++i) {
       const int c = tid + i * kThreads;
       const int key = c / (D / 8), col = (c % (D / 8)) * 8;
-      const int j = kv0 + key;
-      kreg[i] = (j < n_keys) ? *reinterpret_cast<const u32x4*>(key_src(j, p.k_pre, p.k_blk) + col)
-                             : u32x4{0u, 0u, 0u, 0u};
+      const int j = min(kv0 + key, n_keys - 1);
+      kreg[i] = *reinterpret_cast<const u32x4*>(key_src(j, p.k_pre, p.k_blk) + col);
     }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      const int j = kv0 + 2 * kp + e;
+      const int j = min(kv0 + 2 * kp + e, n_keys - 1);
 #pragma unroll
       for (int c = 0; c < kVd / 8; ++c)
-        vreg[e][c] = (j < n_keys)
-                         ? *reinterpret_cast<const u32x4*>(key_src(j, p.v_pre, p.v_blk) +
-                                                          dg * kVd + 8 * c)
-                         : u32x4{0u, 0u, 0u, 0u};
+        vreg[e][c] = *reinterpret_cast<const u32x4*>(key_src(j, p.v_pre, p.v_blk) + dg * kVd + 8 * c);
     }
   };
-  auto sstore = [&]() {
+  auto sstore = [&](int kv0) {
+    const u32x4 zero{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int i = 0; i < kKPer; ++i) {
       const int c = tid + i * kThreads;
       const int key = c / (D / 8), col = (c % (D / 8)) * 8;
-      *reinterpret_cast<u32x4*>(Ks + key * kKRow + col) = kreg[i];
+      *reinterpret_cast<u32x4*>(Ks + key * kKRow + col) = (kv0 + key < n_keys) ? kreg[i] : zero;
     }
+    const bool ok0 = kv0 + 2 * kp < n_keys, ok1 = kv0 + 2 * kp + 1 < n_keys;
 #pragma unroll
     for (int c = 0; c < kVd / 8; ++c)
 #pragma unroll
@@ -126,8 +126,8 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
         for (int hw = 0; hw < 2; ++hw) {
           const int d = dg * kVd + 8 * c + 2 * w4 + hw;
-          const uint32_t lo = (vreg[0][c][w4] >> (16 * hw)) & 0xffffu;
-          const uint32_t hi = (vreg[1][c][w4] >> (16 * hw)) & 0xffffu;
+          const uint32_t lo = ok0 ? (vreg[0][c][w4] >> (16 * hw)) & 0xffffu : 0u;
+          const uint32_t hi = ok1 ? (vreg[1][c][w4] >> (16 * hw)) & 0xffffu : 0u;
           *reinterpret_cast<uint32_t*>(Vt + d * kVRow + 2 * kp) = lo | (hi << 16);
         }
   };
@@ -137,7 +137,7 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
   for (int st = 0; st < n_stages; ++st) {
     const int kv0 = st * kKeys;
     __syncthreads();  // previous stage's LDS reads are done
-    sstore();
+    sstore(kv0);
     __syncthreads();
     if (st + 1 < n_stages) gload(kv0 + kKeys);
 

@@ -185,14 +185,436 @@ __global__ __launch_bounds__(C::kThreads) void lmhead_bf16_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Streaming kernel for few block positions (n_rows <= 32 * NT).
+//
+// With a handful of positions the product is a bandwidth-bound pass over W.  One workgroup per
+// compute unit owns a contiguous slice of vocabulary rows.  Each of its 8 waves streams its
+// share of the slice from HBM straight into MFMA A-operand registers, keeping kDepth k-steps of
+// loads in flight; h, the B operand shared by all waves, goes through a double-buffered LDS
+// chunk.  Every W byte is read once, by one lane, with no LDS round trip.
+// ---------------------------------------------------------------------------------------
+constexpr int kStreamWaves = 8;
+constexpr int kStreamThreads = kStreamWaves * 64;
+constexpr int kStreamGroups = 256;  // workgroups (one per MI355X compute unit)
+
+template <int TM, int NT, int kDepth>
+__global__ __launch_bounds__(kStreamThreads) void lmhead_stream_kernel(
+    const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
+    int vocab, int rows_per_wg, Partial* __restrict__ part, int n_slices) {
+  constexpr int KC = 512 / NT;         // h columns per LDS chunk
+  constexpr int kPitch = KC + 8;       // LDS row pitch (bf16)
+  constexpr int kSpc = KC / 16;        // k-steps per chunk
+  constexpr int kHRows = NT * 32;
+  constexpr int kHChunks16 = kHRows * KC / 8;  // 16-byte pieces per h chunk
+  constexpr int kHPer = kHChunks16 / kStreamThreads;
+  static_assert(kHChunks16 % kStreamThreads == 0, "h chunk splits evenly");
+  static_assert(kSpc % kDepth == 0, "chunk boundary falls on a group boundary");
+  __shared__ __attribute__((aligned(16))) uint16_t hs[2][kHRows * kPitch];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int wg = blockIdx.x;
+  const int vb = wg * rows_per_wg;
+  const int ve = min(vocab, vb + rows_per_wg);
+  const int rw = (rows_per_wg + kStreamWaves - 1) / kStreamWaves;
+  const int wb = vb + wave * rw;
+  const int we = min(ve, wb + rw);
+
+  // Every global load below is unconditional with a clamped address (a conditional load would
+  // make the compiler wait for it on the spot and serialise the stream).  Lanes past the end
+  // of the wave's rows re-read its last row (a cache hit); their sums are discarded.
+  const int wlast = max(min(we, vocab) - 1, 0);
+  const uint16_t* wp[TM];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int row = min(wb + tm * 32 + l32, wlast);
+    wp[tm] = w + static_cast<size_t>(row) * hidden + 8 * half;
+  }
+  const int nsteps = hidden / 16;
+  // The k-loop runs over whole groups of kDepth steps; steps past the end re-read the last
+  // real step of W (addresses stay in bounds) and meet h columns that are zero in LDS.
+  const int nsteps_p = (nsteps + kDepth - 1) / kDepth * kDepth;
+  const int nchunks = (hidden + KC - 1) / KC;
+
+  u32x4 buf[kDepth][TM];
+  auto issue = [&](int j, int step) {
+    const int st = min(step, nsteps - 1);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) buf[j][tm] = *reinterpret_cast<const u32x4*>(wp[tm] + 16 * st);
+  };
+
+  // h pieces: rows past n_rows re-read row n_rows - 1 (their columns of the product are
+  // discarded); columns past hidden are zeroed when stored to LDS.
+  u32x4 hreg[kHPer];
+  auto load_h = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < kHPer; ++i) {
+      const int idx = tid + i * kStreamThreads;
+      const int row = min(idx / (KC / 8), n_rows - 1);
+      const int col = min(c * KC + (idx % (KC / 8)) * 8, hidden - 8);
+      hreg[i] = *reinterpret_cast<const u32x4*>(h + static_cast<size_t>(row) * hidden + col);
+    }
+  };
+  auto store_h = [&](int b, int c) {
+#pragma unroll
+    for (int i = 0; i < kHPer; ++i) {
+      const int idx = tid + i * kStreamThreads;
+      const int row = idx / (KC / 8), col = (idx % (KC / 8)) * 8;
+      const bool ok = c * KC + col < hidden;
+      *reinterpret_cast<u32x4*>(&hs[b][row * kPitch + col]) = ok ? hreg[i] : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+
+  f32x16 acc[TM][NT];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < NT; ++b) acc[a][b] = f32x16{};
+
+#pragma unroll
+  for (int j = 0; j < kDepth; ++j) issue(j, j);
+  load_h(0);
+  store_h(0, 0);
+  __syncthreads();
+  if (nchunks > 1) load_h(1);
+
+  auto consume = [&](int g, int j) {
+    const uint16_t* hb = hs[(g / kSpc) & 1] + (g % kSpc) * 16 + 8 * half + 16 * j;
+    bf16x8 b[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      b[nt] = *reinterpret_cast<const bf16x8*>(hb + (nt * 32 + l32) * kPitch);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, buf[j][tm]);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[tm][nt] = mfma32(a, b[nt], acc[tm][nt]);
+    }
+  };
+  auto chunk_boundary = [&](int g) {
+    if (g > 0 && g % kSpc == 0) {
+      // Entering chunk c: its h pieces were fetched during chunk c-1; the buffer they go to
+      // was last read during chunk c-2, before the barrier that opened chunk c-1.
+      const int c = g / kSpc;
+      store_h(c & 1, c);
+      __syncthreads();
+      if (c + 1 < nchunks) load_h(c + 1);
+    }
+  };
+
+  for (int g = 0; g < nsteps_p - kDepth; g += kDepth) {
+    chunk_boundary(g);
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j) {
+      consume(g, j);
+      issue(j, g + kDepth + j);
+    }
+  }
+  chunk_boundary(nsteps_p - kDepth);
+#pragma unroll
+  for (int j = 0; j < kDepth; ++j) consume(nsteps_p - kDepth, j);
+
+  // Epilogue: per-lane partial over this wave's rows for its position, then across waves.
+  __syncthreads();  // all h reads done; reuse LDS for the cross-wave reduction
+  Partial* red = reinterpret_cast<Partial*>(&hs[0][0]);  // [kStreamWaves][kHRows]
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float m = kNegBig;
+    int32_t idx = kNoIndex;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = wb + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const float z = acc[tm][nt][r];
+        if (v < we && z > m) {
+          m = z;
+          idx = v;
+        }
+      }
+    float s = 0.f, t = 0.f;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = wb + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (v < we) {
+          const float y = (acc[tm][nt][r] - m) * kLog2e;
+          const float e = fast_exp2(y);
+          s += e;
+          t = fmaf(e, y, t);
+        }
+      }
+    Partial p{m, s, t, idx};
+    p = partial_xor_merge(p, 32, lane);
+    if (lane < 32) red[wave * kHRows + nt * 32 + l32] = p;
+  }
+  __syncthreads();
+  if (tid < kHRows && tid < n_rows) {
+    Partial p = red[tid];
+#pragma unroll
+    for (int k = 1; k < kStreamWaves; ++k) p = partial_merge(p, red[k * kHRows + tid]);
+    part[static_cast<size_t>(tid) * n_slices + wg] = p;
+  }
+}
+
+// Same streaming scheme on 16x16x32 MFMA tiles.  A lane of the A operand holds 8 consecutive
+// k-values of row l % 16 and the four lanes of a row cover 64 contiguous bytes, so each load
+// instruction reads 16 rows x 64 B of W (twice the run length of the 32x32 layout).
+// Lane l of the f32x4 accumulator holds C[4 (l / 16) + r][l % 16].
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+template <int TM, int NT, int kDepth>  // TM 16-row tiles per wave, NT 16-position tiles
+__global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
+    const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
+    int vocab, int rows_per_wg, Partial* __restrict__ part, int n_slices) {
+  constexpr int KC = 1024 / NT;        // h columns per LDS chunk
+  constexpr int kPitch = KC + 8;       // LDS row pitch (bf16)
+  constexpr int kSpc = KC / 32;        // k-steps per chunk
+  constexpr int kHRows = NT * 16;
+  constexpr int kHChunks16 = kHRows * KC / 8;
+  constexpr int kHPer = kHChunks16 / kStreamThreads;
+  static_assert(kHChunks16 % kStreamThreads == 0, "h chunk splits evenly");
+  static_assert(kSpc % kDepth == 0, "chunk boundary falls on a group boundary");
+  __shared__ __attribute__((aligned(16))) uint16_t hs[2][kHRows * kPitch];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = lane >> 4, l16 = lane & 15;
+  const int wg = blockIdx.x;
+  const int vb = wg * rows_per_wg;
+  const int ve = min(vocab, vb + rows_per_wg);
+  const int rw = (rows_per_wg + kStreamWaves - 1) / kStreamWaves;
+  const int wb = vb + wave * rw;
+  const int we = min(ve, wb + rw);
+
+  // Unconditional loads with clamped addresses, as in the 32x32 kernel.
+  const int wlast = max(min(we, vocab) - 1, 0);
+  const uint16_t* wp[TM];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int row = min(wb + tm * 16 + l16, wlast);
+    wp[tm] = w + static_cast<size_t>(row) * hidden + 8 * grp;
+  }
+  const int nsteps = hidden / 32;
+  const int nsteps_p = (nsteps + kDepth - 1) / kDepth * kDepth;
+  const int nchunks = (hidden + KC - 1) / KC;
+
+  u32x4 buf[kDepth][TM];
+  auto issue = [&](int j, int step) {
+    const int st = min(step, nsteps - 1);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) buf[j][tm] = *reinterpret_cast<const u32x4*>(wp[tm] + 32 * st);
+  };
+  u32x4 hreg[kHPer];
+  auto load_h = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < kHPer; ++i) {
+      const int idx = tid + i * kStreamThreads;
+      const int row = min(idx / (KC / 8), n_rows - 1);
+      const int col = min(c * KC + (idx % (KC / 8)) * 8, hidden - 8);
+      hreg[i] = *reinterpret_cast<const u32x4*>(h + static_cast<size_t>(row) * hidden + col);
+    }
+  };
+  auto store_h = [&](int b, int c) {
+#pragma unroll
+    for (int i = 0; i < kHPer; ++i) {
+      const int idx = tid + i * kStreamThreads;
+      const int row = idx / (KC / 8), col = (idx % (KC / 8)) * 8;
+      const bool ok = c * KC + col < hidden;
+      *reinterpret_cast<u32x4*>(&hs[b][row * kPitch + col]) = ok ? hreg[i] : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+
+  f32x4 acc[TM][NT];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < NT; ++b) acc[a][b] = f32x4{};
+
+#pragma unroll
+  for (int j = 0; j < kDepth; ++j) issue(j, j);
+  load_h(0);
+  store_h(0, 0);
+  __syncthreads();
+  if (nchunks > 1) load_h(1);
+
+  auto consume = [&](int g, int j) {
+    const uint16_t* hb = hs[(g / kSpc) & 1] + (g % kSpc) * 32 + 8 * grp + 32 * j;
+    bf16x8 b[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      b[nt] = *reinterpret_cast<const bf16x8*>(hb + (nt * 16 + l16) * kPitch);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, buf[j][tm]);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[tm][nt] = mfma16(a, b[nt], acc[tm][nt]);
+    }
+  };
+  auto chunk_boundary = [&](int g) {
+    if (g > 0 && g % kSpc == 0) {
+      const int c = g / kSpc;
+      store_h(c & 1, c);
+      __syncthreads();
+      if (c + 1 < nchunks) load_h(c + 1);
+    }
+  };
+
+  for (int g = 0; g < nsteps_p - kDepth; g += kDepth) {
+    chunk_boundary(g);
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j) {
+      consume(g, j);
+      issue(j, g + kDepth + j);
+    }
+  }
+  chunk_boundary(nsteps_p - kDepth);
+#pragma unroll
+  for (int j = 0; j < kDepth; ++j) consume(nsteps_p - kDepth, j);
+
+  __syncthreads();
+  Partial* red = reinterpret_cast<Partial*>(&hs[0][0]);  // [kStreamWaves][kHRows]
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float m = kNegBig;
+    int32_t idx = kNoIndex;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int v = wb + tm * 16 + 4 * grp + r;
+        const float z = acc[tm][nt][r];
+        if (v < we && z > m) {
+          m = z;
+          idx = v;
+        }
+      }
+    float s = 0.f, t = 0.f;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int v = wb + tm * 16 + 4 * grp + r;
+        if (v < we) {
+          const float y = (acc[tm][nt][r] - m) * kLog2e;
+          const float e = fast_exp2(y);
+          s += e;
+          t = fmaf(e, y, t);
+        }
+      }
+    Partial p{m, s, t, idx};
+    p = partial_xor_merge(p, 16, lane);
+    p = partial_xor_merge(p, 32, lane);
+    if (lane < 16) red[wave * kHRows + nt * 16 + l16] = p;
+  }
+  __syncthreads();
+  if (tid < kHRows && tid < n_rows) {
+    Partial p = red[tid];
+#pragma unroll
+    for (int k = 1; k < kStreamWaves; ++k) p = partial_merge(p, red[k * kHRows + tid]);
+    part[static_cast<size_t>(tid) * n_slices + wg] = p;
+  }
+}
+
+// Streaming variant: MFMA tile shape (16 = 16x16x32, 32 = 32x32x16) and k-steps of W loads
+// in flight per wave.  Defaults come from measurement on MI355X (see the build notes); the
+// macros exist so that other settings can be built and timed.
+#ifndef EB_STREAM_SHAPE
+#define EB_STREAM_SHAPE 16
+#endif
+#ifndef EB_STREAM_DEPTH
+#define EB_STREAM_DEPTH 2
+#endif
+constexpr int kStreamShape = EB_STREAM_SHAPE;
+constexpr int kStreamDepth = EB_STREAM_DEPTH;
+static_assert(kStreamShape == 16 || kStreamShape == 32, "EB_STREAM_SHAPE is 16 or 32");
+
+struct StreamPlan {
+  int groups, rows_per_wg, tm;  // tm: MFMA row tiles per wave
+};
+
+StreamPlan stream_plan(int vocab) {
+  const int groups = min(kStreamGroups, (vocab + 31) / 32);
+  const int rows = (vocab + groups - 1) / groups;
+  const int rw = (rows + kStreamWaves - 1) / kStreamWaves;
+  return StreamPlan{groups, rows, (rw + kStreamShape - 1) / kStreamShape};
+}
+
+constexpr int kStreamMaxRows = 64;  // n_rows handled by the streaming kernel
+constexpr int kStreamMaxTm = kStreamShape == 16 ? 8 : 4;
+
+bool use_stream(int n_rows, int vocab) {
+  if (n_rows > kStreamMaxRows) return false;
+  const int tm = stream_plan(vocab).tm;
+  if (n_rows > 2 * kStreamShape) return tm <= (kStreamShape == 16 ? 6 : 3);  // register budget
+  return tm <= kStreamMaxTm;
+}
+
+template <int TM, int NT>
+hipError_t launch_stream_tm(int n_rows, int hidden, int vocab, const StreamPlan& pl,
+                            const void* h, const void* w, Partial* part, hipStream_t s) {
+  if constexpr (kStreamShape == 16) {
+    constexpr int D = (kStreamDepth * TM > 16) ? (16 / TM > 0 ? 16 / TM : 1) : kStreamDepth;
+    constexpr int Dp = D >= 4 ? 4 : (D >= 2 ? 2 : 1);  // divides the per-chunk step count
+    hipLaunchKernelGGL((lmhead_stream16_kernel<TM, NT, Dp>), dim3(pl.groups),
+                       dim3(kStreamThreads), 0, s, static_cast<const uint16_t*>(h),
+                       static_cast<const uint16_t*>(w), n_rows, hidden, vocab, pl.rows_per_wg,
+                       part, pl.groups);
+  } else {
+    constexpr int D = (kStreamDepth * TM > 16) ? (16 / TM) : kStreamDepth;
+    constexpr int Dp = D >= 8 ? 8 : (D >= 4 ? 4 : 2);
+    hipLaunchKernelGGL((lmhead_stream_kernel<TM, NT, Dp>), dim3(pl.groups), dim3(kStreamThreads),
+                       0, s, static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w),
+                       n_rows, hidden, vocab, pl.rows_per_wg, part, pl.groups);
+  }
+  return hipGetLastError();
+}
+
+// NT: position tiles (of 16 or 32 positions) covering n_rows.
+template <int NT>
+hipError_t launch_stream(int n_rows, int hidden, int vocab, const void* h, const void* w,
+                         Partial* part, hipStream_t s) {
+  const StreamPlan pl = stream_plan(vocab);
+  switch (pl.tm) {
+    case 1: return launch_stream_tm<1, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
+    case 2: return launch_stream_tm<2, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
+    case 3: return launch_stream_tm<3, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
+    case 4:
+      if constexpr (kStreamShape == 16 || NT == 1)
+        return launch_stream_tm<4, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
+      return hipErrorInvalidValue;
+    case 5:
+    case 6:
+    case 7:
+    case 8:
+      if constexpr (kStreamShape == 16) {
+        if (pl.tm == 5) return launch_stream_tm<5, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
+        if (pl.tm == 6) return launch_stream_tm<6, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
+        if (pl.tm == 7) return launch_stream_tm<7, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
+        return launch_stream_tm<8, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
+      }
+      return hipErrorInvalidValue;
+    default: return hipErrorInvalidValue;  // excluded by use_stream
+  }
+}
+
+hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, const void* w,
+                              Partial* part, hipStream_t s) {
+  constexpr int kTile = kStreamShape;
+  if (n_rows <= kTile) return launch_stream<1>(n_rows, hidden, vocab, h, w, part, s);
+  if (n_rows <= 2 * kTile) return launch_stream<2>(n_rows, hidden, vocab, h, w, part, s);
+  if constexpr (kStreamShape == 16) {
+    if (n_rows <= 4 * kTile) return launch_stream<4>(n_rows, hidden, vocab, h, w, part, s);
+  }
+  return hipErrorInvalidValue;  // excluded by use_stream
+}
+
 // Tile shapes: vocabulary rows per workgroup x block positions per workgroup.
-using TileNarrow = LmTile<128, 32, 64, 4, 1>;   // n_rows <= 32 (batch-1 step): W streamed once
-using TileMid = LmTile<128, 64, 64, 4, 1>;      // n_rows <= 64
-using TileWide = LmTile<128, 128, 32, 2, 2>;    // larger batches
-constexpr int kBf16SliceRows = 128;             // every bf16 tile shape uses BM = 128
-static_assert(TileNarrow::BM == kBf16SliceRows && TileMid::BM == kBf16SliceRows &&
-                  TileWide::BM == kBf16SliceRows,
-              "slice count depends on BM only");
+using TileWide = LmTile<128, 128, 32, 2, 2>;    // n_rows > kStreamMaxRows
+constexpr int kBf16SliceRows = TileWide::BM;
 
 template <class C>
 hipError_t launch_bf16(int n_rows, int hidden, int vocab, const void* h, const void* w,
@@ -265,7 +687,7 @@ __global__ __launch_bounds__(256) void lmhead_combine_kernel(const Partial* __re
 }  // namespace
 
 int lmhead_num_slices(bool bf16, int n_rows, int vocab) {
-  (void)n_rows;
+  if (bf16 && use_stream(n_rows, vocab)) return stream_plan(vocab).groups;
   const int rows = bf16 ? kBf16SliceRows : kF32SliceRows;
   return (vocab + rows - 1) / rows;
 }
@@ -285,8 +707,7 @@ hipError_t lmhead_partials(bool bf16, int n_rows, int hidden, int vocab, const v
                        static_cast<const float*>(w), n_rows, hidden, vocab, n_slices, part);
     return hipGetLastError();
   }
-  if (n_rows <= 32) return launch_bf16<TileNarrow>(n_rows, hidden, vocab, h, w, part, n_slices, s);
-  if (n_rows <= 64) return launch_bf16<TileMid>(n_rows, hidden, vocab, h, w, part, n_slices, s);
+  if (use_stream(n_rows, vocab)) return launch_stream_rows(n_rows, hidden, vocab, h, w, part, s);
   return launch_bf16<TileWide>(n_rows, hidden, vocab, h, w, part, n_slices, s);
 }
 

@@ -59,6 +59,13 @@ LM_CASES = [
     (64, 192, 4099, "bf16"),
     (65, 256, 2500, "bf16"),
     (200, 512, 5000, "bf16"),
+    # streaming kernel: 1..4 row tiles per wave, partial h chunks
+    (32, 256, 126464, "bf16"),
+    (17, 128, 152064, "bf16"),
+    (48, 192, 152064, "bf16"),
+    (8, 64, 200000, "bf16"),
+    (40, 1600, 9000, "bf16"),
+    (3, 4160, 20000, "bf16"),
     (32, 256, 2048, "f32"),
     (7, 100, 999, "f32"),
 ]
