@@ -15,177 +15,6 @@ namespace eb {
 namespace {
 
 // ---------------------------------------------------------------------------------------
-// bf16 MFMA kernel
-// ---------------------------------------------------------------------------------------
-template <int BM_, int BN_, int BK_, int WM_, int WN_>
-struct LmTile {
-  static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_;
-  static constexpr int kThreads = WM * WN * 64;
-  static constexpr int kWaveM = BM / WM;
-  static constexpr int kWaveN = BN / WN;
-  static constexpr int TM = kWaveM / 32;
-  static constexpr int TN = kWaveN / 32;
-  static constexpr int kRow = BK + 8;             // LDS row pitch in bf16 (16 B of padding)
-  static constexpr int kStage = (BM + BN) * kRow;  // bf16 elements per pipeline stage
-  static constexpr int kChunksA = BM * (BK / 8);   // 16-byte chunks per stage
-  static constexpr int kChunksB = BN * (BK / 8);
-  static constexpr int kPerA = kChunksA / kThreads;
-  static constexpr int kPerB = (kChunksB + kThreads - 1) / kThreads;
-  static constexpr int kLdsBytes = 2 * kStage * 2;
-  static_assert(BM % (32 * WM) == 0 && BN % (32 * WN) == 0, "wave tile must be 32-aligned");
-  static_assert(kChunksA % kThreads == 0, "A tile must split evenly over threads");
-  static_assert(BK == 32 || BK == 64, "BK");
-  static_assert(kLdsBytes <= 65536, "LDS budget");
-  static_assert(WM * BN * (int)sizeof(Partial) <= kLdsBytes, "reduction scratch fits in LDS");
-};
-
-template <class C>
-__global__ __launch_bounds__(C::kThreads) void lmhead_bf16_kernel(
-    const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
-    int vocab, int n_slices, Partial* __restrict__ part) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::kStage];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave % C::WM;
-  const int wn = wave / C::WM;
-  const int vt = blockIdx.x;
-  const int v0 = vt * C::BM;
-  const int r0 = blockIdx.y * C::BN;
-
-  // Per-thread 16-byte chunks of each stage: chunk c covers row c / (BK/8), columns
-  // 8 * (c % (BK/8)) .. +7.  Rows past the end are clamped to a valid row; their results are
-  // discarded in the epilogue.
-  constexpr int kCpr = C::BK / 8;
-  const uint16_t* ga[C::kPerA];
-  int la[C::kPerA];
-#pragma unroll
-  for (int i = 0; i < C::kPerA; ++i) {
-    const int c = tid + i * C::kThreads;
-    const int row = c / kCpr, col = (c % kCpr) * 8;
-    const int v = min(v0 + row, vocab - 1);
-    ga[i] = w + static_cast<size_t>(v) * hidden + col;
-    la[i] = row * C::kRow + col;
-  }
-  const uint16_t* gb[C::kPerB];
-  int lb[C::kPerB];
-  bool okb[C::kPerB];
-#pragma unroll
-  for (int i = 0; i < C::kPerB; ++i) {
-    const int c = tid + i * C::kThreads;
-    okb[i] = c < C::kChunksB;
-    const int cc = okb[i] ? c : 0;
-    const int row = cc / kCpr, col = (cc % kCpr) * 8;
-    const int r = min(r0 + row, n_rows - 1);
-    gb[i] = h + static_cast<size_t>(r) * hidden + col;
-    lb[i] = C::BM * C::kRow + row * C::kRow + col;
-  }
-
-  u32x4 ra[C::kPerA], rb[C::kPerB];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < C::kPerA; ++i) ra[i] = *reinterpret_cast<const u32x4*>(ga[i] + k0);
-#pragma unroll
-    for (int i = 0; i < C::kPerB; ++i)
-      if (okb[i]) rb[i] = *reinterpret_cast<const u32x4*>(gb[i] + k0);
-  };
-  auto sstore = [&](int st) {
-    uint16_t* base = smem + st * C::kStage;
-#pragma unroll
-    for (int i = 0; i < C::kPerA; ++i) *reinterpret_cast<u32x4*>(base + la[i]) = ra[i];
-#pragma unroll
-    for (int i = 0; i < C::kPerB; ++i)
-      if (okb[i]) *reinterpret_cast<u32x4*>(base + lb[i]) = rb[i];
-  };
-
-  f32x16 acc[C::TM][C::TN];
-#pragma unroll
-  for (int a = 0; a < C::TM; ++a)
-#pragma unroll
-    for (int b = 0; b < C::TN; ++b) acc[a][b] = f32x16{};
-
-  // The contraction index inside a stage is permuted so that each lane reads one contiguous
-  // run of its row: MFMA step s, lane half hf uses columns (BK/2)*hf + 8*s .. +7 for both
-  // operands.  Any permutation applied to both operands leaves W h unchanged.
-  const int half = lane >> 5;
-  const int l32 = lane & 31;
-  const int nk = hidden / C::BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * C::BK);
-    const uint16_t* Ab = smem + cur * C::kStage;
-    const uint16_t* Bb = Ab + C::BM * C::kRow;
-#pragma unroll
-    for (int s = 0; s < C::BK / 16; ++s) {
-      const int koff = (C::BK / 2) * half + 8 * s;
-      bf16x8 a[C::TM], b[C::TN];
-#pragma unroll
-      for (int tm = 0; tm < C::TM; ++tm)
-        a[tm] = *reinterpret_cast<const bf16x8*>(
-            Ab + (wm * C::kWaveM + tm * 32 + l32) * C::kRow + koff);
-#pragma unroll
-      for (int tn = 0; tn < C::TN; ++tn)
-        b[tn] = *reinterpret_cast<const bf16x8*>(
-            Bb + (wn * C::kWaveN + tn * 32 + l32) * C::kRow + koff);
-#pragma unroll
-      for (int tm = 0; tm < C::TM; ++tm)
-#pragma unroll
-        for (int tn = 0; tn < C::TN; ++tn) acc[tm][tn] = mfma32(a[tm], b[tn], acc[tm][tn]);
-    }
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
-  }
-
-  // Epilogue: each lane reduces the logits it holds for its column (one block position).
-  Partial* red = reinterpret_cast<Partial*>(smem);  // [WM][BN]
-#pragma unroll
-  for (int tn = 0; tn < C::TN; ++tn) {
-    float m = kNegBig;
-    int32_t idx = kNoIndex;
-#pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = v0 + wm * C::kWaveM + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        const float z = acc[tm][tn][r];
-        if (v < vocab && z > m) {  // ascending v: strict > keeps the lowest index
-          m = z;
-          idx = v;
-        }
-      }
-    // y = (z - m) log2 e is exactly 0 at the maximum, so s >= 1 and kappa = 1/s <= 1.
-    float s = 0.f, t = 0.f;
-#pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = v0 + wm * C::kWaveM + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (v < vocab) {
-          const float y = (acc[tm][tn][r] - m) * kLog2e;
-          const float e = fast_exp2(y);
-          s += e;
-          t = fmaf(e, y, t);
-        }
-      }
-    Partial p{m, s, t, idx};
-    p = partial_xor_merge(p, 32, lane);
-    if (lane < 32) red[wm * C::BN + wn * C::kWaveN + tn * 32 + l32] = p;
-  }
-  __syncthreads();
-  for (int c = tid; c < C::BN; c += C::kThreads) {
-    Partial p = red[c];
-#pragma unroll
-    for (int k = 1; k < C::WM; ++k) p = partial_merge(p, red[k * C::BN + c]);
-    const int row = r0 + c;
-    if (row < n_rows) part[static_cast<size_t>(row) * n_slices + vt] = p;
-  }
-}
-
-// ---------------------------------------------------------------------------------------
 // Streaming kernel for few block positions (n_rows <= 32 * NT).
 //
 // With a handful of positions the product is a bandwidth-bound pass over W.  One workgroup per
@@ -612,17 +441,180 @@ hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, 
   return hipErrorInvalidValue;  // excluded by use_stream
 }
 
-// Tile shapes: vocabulary rows per workgroup x block positions per workgroup.
-using TileWide = LmTile<128, 128, 32, 2, 2>;    // n_rows > kStreamMaxRows
-constexpr int kBf16SliceRows = TileWide::BM;
+// ---------------------------------------------------------------------------------------
+// Large-batch kernel: 256 (vocabulary) x 256 (positions) tiles.
+//
+// 8 waves in a 2 x 4 grid, each a 128 x 64 sub-tile of 4 x 2 32x32x16 MFMA blocks; BK = 64 per
+// LDS stage, LDS double buffer, next stage prefetched into registers.  Launch order is
+// XCD-aware: vocabulary tiles are grouped in bands of kBand, band b goes to XCD b % 8
+// (workgroups are dealt to the 8 XCDs round-robin by id), and each XCD sweeps a band row tile
+// by row tile, so the ~32 workgroups an XCD runs at once share kBand W tiles and about 8 h tiles
+// in its L2, and each W tile is fetched from HBM about once.
+// ---------------------------------------------------------------------------------------
+constexpr int kWideBM = 256, kWideBN = 256, kWideBK = 64;
+constexpr int kWideThreads = 512;
+constexpr int kXcds = 8;
+constexpr int kBand = 4;
 
-template <class C>
-hipError_t launch_bf16(int n_rows, int hidden, int vocab, const void* h, const void* w,
-                       Partial* part, int n_slices, hipStream_t s) {
-  dim3 grid(n_slices, (n_rows + C::BN - 1) / C::BN);
-  hipLaunchKernelGGL(lmhead_bf16_kernel<C>, grid, dim3(C::kThreads), 0, s,
+struct WideMap {
+  int n_vtiles, n_rtiles, n_bands, grid;
+};
+
+WideMap wide_map(int n_rows, int vocab) {
+  WideMap m;
+  m.n_vtiles = (vocab + kWideBM - 1) / kWideBM;
+  m.n_rtiles = (n_rows + kWideBN - 1) / kWideBN;
+  m.n_bands = (m.n_vtiles + kBand - 1) / kBand;
+  const int bands_per_xcd = (m.n_bands + kXcds - 1) / kXcds;
+  m.grid = kXcds * bands_per_xcd * kBand * m.n_rtiles;
+  return m;
+}
+
+__global__ __launch_bounds__(kWideThreads) void lmhead_wide_kernel(
+    const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
+    int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part) {
+  constexpr int BM = kWideBM, BN = kWideBN, BK = kWideBK;
+  constexpr int WM = 2, WN = 4, kWaveM = BM / WM, kWaveN = BN / WN;
+  constexpr int TM = kWaveM / 32, TN = kWaveN / 32;
+  constexpr int kRow = BK + 8;              // LDS pitch (bf16): 144 B, conflict-free b128 reads
+  constexpr int kStage = (BM + BN) * kRow;  // bf16 per stage
+  constexpr int kCpr = BK / 8;              // 16-byte chunks per row per stage
+  constexpr int kPer = (BM + BN) * kCpr / kWideThreads;
+  static_assert((BM + BN) * kCpr % kWideThreads == 0, "stage splits evenly");
+  static_assert(BM * kCpr % kWideThreads == 0, "A and B chunks do not share a thread slot");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
+
+  // tile of this workgroup
+  const int id = blockIdx.x;
+  const int xcd = id % kXcds, k = id / kXcds;
+  const int per_band = kBand * n_rtiles;
+  const int band = xcd + kXcds * (k / per_band);
+  if (band >= n_bands) return;
+  const int t = k % per_band;
+  const int nv = min(kBand, n_vtiles - band * kBand);
+  if (t >= nv * n_rtiles) return;
+  const int vt = band * kBand + t % nv;
+  const int rt = t / nv;
+  const int v0 = vt * BM, r0 = rt * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int half = lane >> 5, l32 = lane & 31;
+
+  // Loader: chunk c < BM*kCpr is an A (W) chunk, the rest are B (h) chunks; rows past the end
+  // are clamped (their products are discarded).
+  const uint16_t* gsrc[kPer];
+  int lds_off[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int c = tid + i * kWideThreads;
+    const bool is_a = c < BM * kCpr;
+    const int cc = is_a ? c : c - BM * kCpr;
+    const int row = cc / kCpr, col = (cc % kCpr) * 8;
+    if (is_a) {
+      gsrc[i] = w + static_cast<size_t>(min(v0 + row, vocab - 1)) * hidden + col;
+      lds_off[i] = row * kRow + col;
+    } else {
+      gsrc[i] = h + static_cast<size_t>(min(r0 + row, n_rows - 1)) * hidden + col;
+      lds_off[i] = (BM + row) * kRow + col;
+    }
+  }
+  u32x4 stage_regs[kPer];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) stage_regs[i] = *reinterpret_cast<const u32x4*>(gsrc[i] + k0);
+  };
+  auto sstore = [&](int st) {
+    uint16_t* base = smem + st * kStage;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) *reinterpret_cast<u32x4*>(base + lds_off[i]) = stage_regs[i];
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b) acc[a][b] = f32x16{};
+
+  const int nk = hidden / BK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * BK);
+    const uint16_t* Ab = smem + cur * kStage + (wm * kWaveM + l32) * kRow;
+    const uint16_t* Bb = smem + cur * kStage + (BM + wn * kWaveN + l32) * kRow;
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      const int koff = (BK / 2) * half + 8 * s;  // same permutation of k for both operands
+      bf16x8 a[TM], b[TN];
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+        a[tm] = *reinterpret_cast<const bf16x8*>(Ab + tm * 32 * kRow + koff);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        b[tn] = *reinterpret_cast<const bf16x8*>(Bb + tn * 32 * kRow + koff);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32(a[tm], b[tn], acc[tm][tn]);
+    }
+    if (kt + 1 < nk) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue: per-lane partial for its position column over 4 x 16 vocabulary rows, merged
+  // with the other half of the wave, then with the other vocabulary wave through LDS.
+  Partial* red = reinterpret_cast<Partial*>(smem);  // [WM][BN]
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    float m = kNegBig;
+    int32_t idx = kNoIndex;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = v0 + wm * kWaveM + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const float z = acc[tm][tn][r];
+        if (v < vocab && z > m) {
+          m = z;
+          idx = v;
+        }
+      }
+    float s = 0.f, tt = 0.f;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = v0 + wm * kWaveM + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (v < vocab) {
+          const float y = (acc[tm][tn][r] - m) * kLog2e;
+          const float e = fast_exp2(y);
+          s += e;
+          tt = fmaf(e, y, tt);
+        }
+      }
+    Partial p{m, s, tt, idx};
+    p = partial_xor_merge(p, 32, lane);
+    if (lane < 32) red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
+  }
+  __syncthreads();
+  if (tid < BN) {
+    Partial p = red[tid];
+#pragma unroll
+    for (int q = 1; q < WM; ++q) p = partial_merge(p, red[q * BN + tid]);
+    const int row = r0 + tid;
+    if (row < n_rows) part[static_cast<size_t>(row) * n_vtiles + vt] = p;
+  }
+}
+
+hipError_t launch_wide(int n_rows, int hidden, int vocab, const void* h, const void* w,
+                       Partial* part, hipStream_t s) {
+  const WideMap m = wide_map(n_rows, vocab);
+  hipLaunchKernelGGL(lmhead_wide_kernel, dim3(m.grid), dim3(kWideThreads), 0, s,
                      static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w), n_rows,
-                     hidden, vocab, n_slices, part);
+                     hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
   return hipGetLastError();
 }
 
@@ -688,8 +680,8 @@ __global__ __launch_bounds__(256) void lmhead_combine_kernel(const Partial* __re
 
 int lmhead_num_slices(bool bf16, int n_rows, int vocab) {
   if (bf16 && use_stream(n_rows, vocab)) return stream_plan(vocab).groups;
-  const int rows = bf16 ? kBf16SliceRows : kF32SliceRows;
-  return (vocab + rows - 1) / rows;
+  if (bf16) return wide_map(n_rows, vocab).n_vtiles;
+  return (vocab + kF32SliceRows - 1) / kF32SliceRows;
 }
 
 size_t lmhead_ws_bytes(bool bf16, int n_rows, int vocab) {
@@ -700,15 +692,15 @@ hipError_t lmhead_partials(bool bf16, int n_rows, int hidden, int vocab, const v
                            const void* w, void* ws, hipStream_t s) {
   if (n_rows == 0) return hipSuccess;
   Partial* part = static_cast<Partial*>(ws);
-  const int n_slices = lmhead_num_slices(bf16, n_rows, vocab);
   if (!bf16) {
+    const int n_slices = lmhead_num_slices(false, n_rows, vocab);
     dim3 grid(n_slices, n_rows);
     hipLaunchKernelGGL(lmhead_f32_kernel, grid, dim3(256), 0, s, static_cast<const float*>(h),
                        static_cast<const float*>(w), n_rows, hidden, vocab, n_slices, part);
     return hipGetLastError();
   }
   if (use_stream(n_rows, vocab)) return launch_stream_rows(n_rows, hidden, vocab, h, w, part, s);
-  return launch_bf16<TileWide>(n_rows, hidden, vocab, h, w, part, n_slices, s);
+  return launch_wide(n_rows, hidden, vocab, h, w, part, s);
 }
 
 hipError_t lmhead_combine(int n_rows, int n_slices, const void* ws, float* conf,

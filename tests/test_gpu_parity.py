@@ -59,6 +59,9 @@ LM_CASES = [
     (64, 192, 4099, "bf16"),
     (65, 256, 2500, "bf16"),
     (200, 512, 5000, "bf16"),
+    # large-batch kernel: several row tiles, vocabulary bands with a partial last band
+    (600, 192, 9000, "bf16"),
+    (300, 128, 1100, "bf16"),
     # streaming kernel: 1..4 row tiles per wave, partial h chunks
     (32, 256, 126464, "bf16"),
     (17, 128, 152064, "bf16"),
