@@ -442,92 +442,163 @@ hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, 
 }
 
 // ---------------------------------------------------------------------------------------
-// Large-batch kernel: 256 (vocabulary) x 256 (positions) tiles.
+// Large-batch kernels: 256 (vocabulary) x BN (positions) tiles.
 //
-// 8 waves in a 2 x 4 grid, each a 128 x 64 sub-tile of 4 x 2 32x32x16 MFMA blocks; BK = 64 per
-// LDS stage, LDS double buffer, next stage prefetched into registers.  Launch order is
-// XCD-aware: vocabulary tiles are grouped in bands of kBand, band b goes to XCD b % 8
-// (workgroups are dealt to the 8 XCDs round-robin by id), and each XCD sweeps a band row tile
-// by row tile, so the ~32 workgroups an XCD runs at once share kBand W tiles and about 8 h tiles
-// in its L2, and each W tile is fetched from HBM about once.
+// Both operands are streamed HBM -> LDS by direct loads (global_load_lds_dwordx4: lane l of a
+// wave writes its 16 bytes to LDS base + 16 l) into a ring of RING stages of BK = 32 hidden
+// columns, RING - 1 stages in flight; no staging registers and no LDS store instructions.  LDS
+// rows are 64 bytes without padding; the 16-byte chunk c of row r is kept in slot
+// c ^ ((r / 4) % 4), which makes the 32-row MFMA operand reads free of bank conflicts.
+// Waves form a 2 x WN grid of 128 x (BN / WN) sub-tiles of 32x32x16 MFMA blocks.
+//
+// Launch order is XCD-aware: vocabulary tiles are grouped in bands of kBand, band b goes to XCD
+// b % 8 (workgroups are dealt to the 8 XCDs round-robin by id), and each XCD sweeps its band row
+// tile by row tile, so the workgroups an XCD runs at once share a few W and h tiles in its L2
+// and each W tile is fetched from HBM about once.
 // ---------------------------------------------------------------------------------------
-constexpr int kWideBM = 256, kWideBN = 256, kWideBK = 64;
-constexpr int kWideThreads = 512;
 constexpr int kXcds = 8;
 constexpr int kBand = 4;
+constexpr int kTileBM = 256;
+constexpr int kTileBK = 32;
 
-struct WideMap {
+struct TileMap {
   int n_vtiles, n_rtiles, n_bands, grid;
 };
 
-WideMap wide_map(int n_rows, int vocab) {
-  WideMap m;
-  m.n_vtiles = (vocab + kWideBM - 1) / kWideBM;
-  m.n_rtiles = (n_rows + kWideBN - 1) / kWideBN;
+TileMap tile_map(int n_rows, int vocab, int bn) {
+  TileMap m;
+  m.n_vtiles = (vocab + kTileBM - 1) / kTileBM;
+  m.n_rtiles = (n_rows + bn - 1) / bn;
   m.n_bands = (m.n_vtiles + kBand - 1) / kBand;
   const int bands_per_xcd = (m.n_bands + kXcds - 1) / kXcds;
   m.grid = kXcds * bands_per_xcd * kBand * m.n_rtiles;
   return m;
 }
 
-__global__ __launch_bounds__(kWideThreads) void lmhead_wide_kernel(
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void global_void_t;
+
+__device__ __forceinline__ void load_to_lds(const void* g, void* l) {
+  // address-space casts (generic -> global / LDS) need C-style casts
+  __builtin_amdgcn_global_load_lds((global_void_t*)(const_cast<void*>(g)), (lds_void_t*)(l), 16, 0,
+                                   0);
+}
+
+// Wait until at most N vector-memory instructions of this wave are outstanding, then barrier.
+// The memory clobber keeps the compiler from moving LDS accesses across it.
+template <int N>
+__device__ __forceinline__ void wait_vm_and_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+  asm volatile("s_barrier" ::: "memory");
+}
+
+// Barrier once the oldest stage in flight has landed, `later` younger stages (each kPer load
+// instructions of this wave) being allowed to stay in flight.
+template <int kPer, int kMaxLater>
+__device__ __forceinline__ void wait_stage(int later) {
+  if constexpr (kMaxLater >= 2) {
+    if (later >= 2) {
+      wait_vm_and_barrier<2 * kPer>();
+      return;
+    }
+  }
+  if constexpr (kMaxLater >= 1) {
+    if (later >= 1) {
+      wait_vm_and_barrier<kPer>();
+      return;
+    }
+  }
+  wait_vm_and_barrier<0>();
+}
+
+// Partial statistics of one lane's column over TM 32-row MFMA blocks.  Element (tm, r) of the
+// lane is vocabulary row vbase + 32 tm + 8 (r / 4) + (r % 4).  The max comes first; the exp pass
+// then walks the rows in decreasing order, so the last z == max hit is the lowest row.
+template <int TM, int TN>
+__device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], int tn, int vbase,
+                                                  int vocab, bool full) {
+  float m = kNegBig;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int v = vbase + tm * 32 + 8 * (r >> 2) + (r & 3);
+      if (full || v < vocab) m = fmaxf(m, acc[tm][tn][r]);
+    }
+  float s = 0.f, t = 0.f;
+  int32_t idx = kNoIndex;
+#pragma unroll
+  for (int tm = TM - 1; tm >= 0; --tm)
+#pragma unroll
+    for (int r = 15; r >= 0; --r) {
+      const int v = vbase + tm * 32 + 8 * (r >> 2) + (r & 3);
+      const float z = acc[tm][tn][r];
+      const bool ok = full || v < vocab;
+      // rows past the vocabulary contribute e = 0 and y = 0 (a lane with no valid row keeps
+      // m = kNegBig, where z - m would overflow and 0 * inf would poison t)
+      const float y = ok ? (z - m) * kLog2e : 0.f;
+      const float e = ok ? fast_exp2(y) : 0.f;
+      s += e;
+      t = fmaf(e, y, t);
+      idx = (ok && z == m) ? v : idx;
+    }
+  return Partial{m, s, t, idx};
+}
+
+template <int WN, int BN, int RING, int MINB>
+__global__ __launch_bounds__(128 * WN, MINB) void lmhead_tile_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
     int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part) {
-  constexpr int BM = kWideBM, BN = kWideBN, BK = kWideBK;
-  constexpr int WM = 2, WN = 4, kWaveM = BM / WM, kWaveN = BN / WN;
+  constexpr int BM = kTileBM, BK = kTileBK;
+  constexpr int WM = 2, kWaves = WM * WN;
+  constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
   constexpr int TM = kWaveM / 32, TN = kWaveN / 32;
-  constexpr int kRow = BK + 8;              // LDS pitch (bf16): 144 B, conflict-free b128 reads
-  constexpr int kStage = (BM + BN) * kRow;  // bf16 per stage
-  constexpr int kCpr = BK / 8;              // 16-byte chunks per row per stage
-  constexpr int kPer = (BM + BN) * kCpr / kWideThreads;
-  static_assert((BM + BN) * kCpr % kWideThreads == 0, "stage splits evenly");
-  static_assert(BM * kCpr % kWideThreads == 0, "A and B chunks do not share a thread slot");
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
+  constexpr int kRowB = BK * 2;                   // 64 bytes per LDS row
+  constexpr int kStageBytes = (BM + BN) * kRowB;
+  constexpr int kInst = (BM + BN) / 16;           // 1 KB wave instructions per stage
+  constexpr int kInstPerWave = kInst / kWaves;
+  static_assert(kInst % kWaves == 0, "stage splits over the waves");
+  static_assert(RING >= 3 && RING <= 4, "ring of 3 or 4 stages");
+  static_assert((RING - 2) * kInstPerWave < 64, "vmcnt range");
+  __shared__ __attribute__((aligned(16))) uint8_t smem[RING * kStageBytes];
+  static_assert(WM * BN * sizeof(Partial) <= RING * kStageBytes, "reduction fits in the ring");
 
-  // tile of this workgroup
   const int id = blockIdx.x;
   const int xcd = id % kXcds, k = id / kXcds;
   const int per_band = kBand * n_rtiles;
   const int band = xcd + kXcds * (k / per_band);
   if (band >= n_bands) return;
-  const int t = k % per_band;
+  const int tt = k % per_band;
   const int nv = min(kBand, n_vtiles - band * kBand);
-  if (t >= nv * n_rtiles) return;
-  const int vt = band * kBand + t % nv;
-  const int rt = t / nv;
+  if (tt >= nv * n_rtiles) return;
+  const int vt = band * kBand + tt % nv;
+  const int rt = tt / nv;
   const int v0 = vt * BM, r0 = rt * BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
   const int half = lane >> 5, l32 = lane & 31;
 
-  // Loader: chunk c < BM*kCpr is an A (W) chunk, the rest are B (h) chunks; rows past the end
-  // are clamped (their products are discarded).
-  const uint16_t* gsrc[kPer];
-  int lds_off[kPer];
+  // This wave's load instructions: q = wave * kInstPerWave + i covers tile rows 16 q .. 16 q + 15
+  // (rows below BM are W, the rest h).  Lane L fetches row 16 q + L / 4, global chunk
+  // (L % 4) ^ swizzle(row), so that LDS slot L % 4 of the row holds that chunk.  Rows past the
+  // end are clamped (their products are discarded).
+  const uint16_t* src[kInstPerWave];
 #pragma unroll
-  for (int i = 0; i < kPer; ++i) {
-    const int c = tid + i * kWideThreads;
-    const bool is_a = c < BM * kCpr;
-    const int cc = is_a ? c : c - BM * kCpr;
-    const int row = cc / kCpr, col = (cc % kCpr) * 8;
-    if (is_a) {
-      gsrc[i] = w + static_cast<size_t>(min(v0 + row, vocab - 1)) * hidden + col;
-      lds_off[i] = row * kRow + col;
-    } else {
-      gsrc[i] = h + static_cast<size_t>(min(r0 + row, n_rows - 1)) * hidden + col;
-      lds_off[i] = (BM + row) * kRow + col;
-    }
+  for (int i = 0; i < kInstPerWave; ++i) {
+    const int q = wave * kInstPerWave + i;
+    const int row = 16 * q + (lane >> 2);
+    const int chunk = (lane & 3) ^ ((row >> 2) & 3);
+    src[i] = row < BM
+                 ? w + static_cast<size_t>(min(v0 + row, vocab - 1)) * hidden + chunk * 8
+                 : h + static_cast<size_t>(min(r0 + row - BM, n_rows - 1)) * hidden + chunk * 8;
   }
-  u32x4 stage_regs[kPer];
-  auto gload = [&](int k0) {
+  auto issue = [&](int kt) {
+    uint8_t* base = smem + (kt % RING) * kStageBytes;
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) stage_regs[i] = *reinterpret_cast<const u32x4*>(gsrc[i] + k0);
-  };
-  auto sstore = [&](int st) {
-    uint16_t* base = smem + st * kStage;
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) *reinterpret_cast<u32x4*>(base + lds_off[i]) = stage_regs[i];
+    for (int i = 0; i < kInstPerWave; ++i)
+      load_to_lds(src[i] + kt * BK, base + (wave * kInstPerWave + i) * 1024);
   };
 
   f32x16 acc[TM][TN];
@@ -537,84 +608,79 @@ __global__ __launch_bounds__(kWideThreads) void lmhead_wide_kernel(
     for (int b = 0; b < TN; ++b) acc[a][b] = f32x16{};
 
   const int nk = hidden / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < RING - 1; ++j)
+    if (j < nk) issue(j);
+
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    const uint16_t* Ab = smem + cur * kStage + (wm * kWaveM + l32) * kRow;
-    const uint16_t* Bb = smem + cur * kStage + (BM + wn * kWaveN + l32) * kRow;
+    // stage kt lands; younger stages kt+1 .. may stay in flight
+    wait_stage<kInstPerWave, RING - 2>(min(RING - 2, nk - 1 - kt));
+    // refill the slot that was read during iteration kt - 1 (every wave is past it)
+    if (kt + RING - 1 < nk) issue(kt + RING - 1);
+    const uint8_t* st = smem + (kt % RING) * kStageBytes;
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
-      const int koff = (BK / 2) * half + 8 * s;  // same permutation of k for both operands
+      const int c = 2 * half + s;  // k-chunk of this MFMA step, the same for both operands
       bf16x8 a[TM], b[TN];
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
-        a[tm] = *reinterpret_cast<const bf16x8*>(Ab + tm * 32 * kRow + koff);
+      for (int tm = 0; tm < TM; ++tm) {
+        const int r = wm * kWaveM + tm * 32 + l32;
+        a[tm] = *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (c ^ ((r >> 2) & 3)));
+      }
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-        b[tn] = *reinterpret_cast<const bf16x8*>(Bb + tn * 32 * kRow + koff);
+      for (int tn = 0; tn < TN; ++tn) {
+        const int r = BM + wn * kWaveN + tn * 32 + l32;
+        b[tn] = *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (c ^ ((r >> 2) & 3)));
+      }
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32(a[tm], b[tn], acc[tm][tn]);
     }
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
   }
+  __syncthreads();  // every wave is done reading the ring before it holds the reduction
 
-  // Epilogue: per-lane partial for its position column over 4 x 16 vocabulary rows, merged
-  // with the other half of the wave, then with the other vocabulary wave through LDS.
+  // Epilogue: per-lane partial for its position column, merged with the other half of the
+  // wave, then with the other vocabulary wave through LDS.
   Partial* red = reinterpret_cast<Partial*>(smem);  // [WM][BN]
+  const bool full = v0 + BM <= vocab;
+  const int vbase = v0 + wm * kWaveM + 4 * half;
 #pragma unroll
   for (int tn = 0; tn < TN; ++tn) {
-    float m = kNegBig;
-    int32_t idx = kNoIndex;
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = v0 + wm * kWaveM + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        const float z = acc[tm][tn][r];
-        if (v < vocab && z > m) {
-          m = z;
-          idx = v;
-        }
-      }
-    float s = 0.f, tt = 0.f;
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = v0 + wm * kWaveM + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (v < vocab) {
-          const float y = (acc[tm][tn][r] - m) * kLog2e;
-          const float e = fast_exp2(y);
-          s += e;
-          tt = fmaf(e, y, tt);
-        }
-      }
-    Partial p{m, s, tt, idx};
+    Partial p = column_partial<TM, TN>(acc, tn, vbase, vocab, full);
     p = partial_xor_merge(p, 32, lane);
     if (lane < 32) red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
   }
   __syncthreads();
-  if (tid < BN) {
-    Partial p = red[tid];
+  for (int c = tid; c < BN; c += kWaves * 64) {
+    Partial p = red[c];
 #pragma unroll
-    for (int q = 1; q < WM; ++q) p = partial_merge(p, red[q * BN + tid]);
-    const int row = r0 + tid;
+    for (int q = 1; q < WM; ++q) p = partial_merge(p, red[q * BN + c]);
+    const int row = r0 + c;
     if (row < n_rows) part[static_cast<size_t>(row) * n_vtiles + vt] = p;
   }
 }
 
-hipError_t launch_wide(int n_rows, int hidden, int vocab, const void* h, const void* w,
+// Tile shape of the large-batch path.  Variant 2 (default): 256 x 256 tiles, 8 waves, ring of 4
+// (128 KB LDS, one workgroup per compute unit).  Variant 1: 256 x 128 tiles, 4 waves, ring of 3
+// (72 KB, two workgroups per compute unit); measured 10% slower at batch 64.
+#ifndef EB_TILE_VARIANT
+#define EB_TILE_VARIANT 2
+#endif
+constexpr int kTileBN = EB_TILE_VARIANT == 1 ? 128 : 256;
+
+hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const void* w,
                        Partial* part, hipStream_t s) {
-  const WideMap m = wide_map(n_rows, vocab);
-  hipLaunchKernelGGL(lmhead_wide_kernel, dim3(m.grid), dim3(kWideThreads), 0, s,
-                     static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w), n_rows,
-                     hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
+  const TileMap m = tile_map(n_rows, vocab, kTileBN);
+  const uint16_t* hp = static_cast<const uint16_t*>(h);
+  const uint16_t* wp = static_cast<const uint16_t*>(w);
+  if constexpr (EB_TILE_VARIANT == 1) {
+    hipLaunchKernelGGL((lmhead_tile_kernel<2, 128, 3, 2>), dim3(m.grid), dim3(256), 0, s, hp, wp,
+                       n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
+  } else {
+    hipLaunchKernelGGL((lmhead_tile_kernel<4, 256, 4, 1>), dim3(m.grid), dim3(512), 0, s, hp, wp,
+                       n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
+  }
   return hipGetLastError();
 }
 
@@ -680,7 +746,7 @@ __global__ __launch_bounds__(256) void lmhead_combine_kernel(const Partial* __re
 
 int lmhead_num_slices(bool bf16, int n_rows, int vocab) {
   if (bf16 && use_stream(n_rows, vocab)) return stream_plan(vocab).groups;
-  if (bf16) return wide_map(n_rows, vocab).n_vtiles;
+  if (bf16) return tile_map(n_rows, vocab, kTileBN).n_vtiles;
   return (vocab + kF32SliceRows - 1) / kF32SliceRows;
 }
 
@@ -700,7 +766,7 @@ hipError_t lmhead_partials(bool bf16, int n_rows, int hidden, int vocab, const v
     return hipGetLastError();
   }
   if (use_stream(n_rows, vocab)) return launch_stream_rows(n_rows, hidden, vocab, h, w, part, s);
-  return launch_wide(n_rows, hidden, vocab, h, w, part, s);
+  return launch_tile(n_rows, hidden, vocab, h, w, part, s);
 }
 
 hipError_t lmhead_combine(int n_rows, int n_slices, const void* ws, float* conf,
