@@ -16,7 +16,7 @@
  *   - Every pointer argument is a DEVICE pointer owned by the caller unless stated
  *     otherwise; descriptor structs themselves live in host memory and are read during the
  *     call only.  The library allocates no device memory and keeps no state besides a
- *     per-thread last-error string and cached device properties.
+ *     per-thread last-error string.
  *   - Every call enqueues work on `stream` (a hipStream_t; NULL = default stream) and
  *     returns without synchronising.  Outputs are valid once the stream reaches them.
  *   - Arguments are checked on the host before anything is launched: a bad argument
@@ -141,7 +141,8 @@ eb_status eb_unmask_select(const eb_ragged* r, const float* conf, const int32_t*
 
 /* ---------------------------------------------------------------------------------------
  * One whole denoising step: eb_block_attn, then eb_lmhead_confidence over the T block rows
- * of h, then eb_unmask_select, enqueued on one stream with no host synchronisation.
+ * of h, then eb_unmask_select, enqueued on `stream` with no host synchronisation.  The
+ * workspace holds the attention's key-split partials followed by the LM-head partials.
  * Field meanings, layouts and requirements are those of the three calls above; the LM-head
  * rows are the block rows (n_rows = ragged.total_block).
  *

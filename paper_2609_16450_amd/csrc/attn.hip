@@ -29,6 +29,12 @@ struct AttnParams {
   const uint16_t* k_pre;
   const uint16_t* v_pre;
   uint16_t* out;
+  // key split: keys of a sequence are cut into ranges of kps keys, one workgroup per range;
+  // with nsplit > 1 the workgroups write unnormalised partials that attn_merge_kernel combines
+  int nsplit, kps;
+  float* o_part;  // [T * hq * nsplit, D]
+  float* m_part;  // [T * hq * nsplit]  running max (log2 units)
+  float* l_part;  // [T * hq * nsplit]  sum of 2^(s - m)
 };
 
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
@@ -45,7 +51,8 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
   __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeys * kKRow];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[D * kVRow];
 
-  const int b = blockIdx.z;
+  const int b = blockIdx.z / p.nsplit;
+  const int sp = blockIdx.z % p.nsplit;
   const int g = blockIdx.y;
   const int G = p.group;
   const int bbeg = p.cu_block[b];
@@ -56,6 +63,9 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
   const int row0 = blockIdx.x * kRowsPerWg;
   if (row0 >= n_rows) return;  // whole workgroup: this tile lies past the block
   const int n_keys = plen + len;
+  const int kbeg = sp * p.kps;
+  if (kbeg >= n_keys) return;  // whole workgroup: this key range lies past the sequence
+  const int kend = min(n_keys, kbeg + p.kps);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
@@ -99,12 +109,12 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
     for (int i = 0; i < kKPer; ++i) {
       const int c = tid + i * kThreads;
       const int key = c / (D / 8), col = (c % (D / 8)) * 8;
-      const int j = min(kv0 + key, n_keys - 1);
+      const int j = min(kv0 + key, kend - 1);
       kreg[i] = *reinterpret_cast<const u32x4*>(key_src(j, p.k_pre, p.k_blk) + col);
     }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      const int j = min(kv0 + 2 * kp + e, n_keys - 1);
+      const int j = min(kv0 + 2 * kp + e, kend - 1);
 #pragma unroll
       for (int c = 0; c < kVd / 8; ++c)
         vreg[e][c] = *reinterpret_cast<const u32x4*>(key_src(j, p.v_pre, p.v_blk) + dg * kVd + 8 * c);
@@ -116,9 +126,9 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
     for (int i = 0; i < kKPer; ++i) {
       const int c = tid + i * kThreads;
       const int key = c / (D / 8), col = (c % (D / 8)) * 8;
-      *reinterpret_cast<u32x4*>(Ks + key * kKRow + col) = (kv0 + key < n_keys) ? kreg[i] : zero;
+      *reinterpret_cast<u32x4*>(Ks + key * kKRow + col) = (kv0 + key < kend) ? kreg[i] : zero;
     }
-    const bool ok0 = kv0 + 2 * kp < n_keys, ok1 = kv0 + 2 * kp + 1 < n_keys;
+    const bool ok0 = kv0 + 2 * kp < kend, ok1 = kv0 + 2 * kp + 1 < kend;
 #pragma unroll
     for (int c = 0; c < kVd / 8; ++c)
 #pragma unroll
@@ -132,10 +142,10 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
         }
   };
 
-  const int n_stages = (n_keys + kKeys - 1) / kKeys;
-  gload(0);
+  const int n_stages = (kend - kbeg + kKeys - 1) / kKeys;
+  gload(kbeg);
   for (int st = 0; st < n_stages; ++st) {
-    const int kv0 = st * kKeys;
+    const int kv0 = kbeg + st * kKeys;
     __syncthreads();  // previous stage's LDS reads are done
     sstore(kv0);
     __syncthreads();
@@ -159,7 +169,7 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = kv0 + kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        const float x = (key < n_keys) ? sacc[kb][r] * p.scale_log2 : -INFINITY;
+        const float x = (key < kend) ? sacc[kb][r] * p.scale_log2 : -INFINITY;
         sacc[kb][r] = x;
         mloc = fmaxf(mloc, x);
       }
@@ -206,6 +216,23 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (!row_ok) return;
+  if (p.nsplit > 1) {
+    const size_t idx = (static_cast<size_t>(bbeg + pos) * p.hq + g * G + hh) * p.nsplit + sp;
+    float* dst = p.o_part + idx * D;
+#pragma unroll
+    for (int db = 0; db < kDBlocks; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = db * 32 + 8 * q4 + 4 * half;
+        *reinterpret_cast<f32x4*>(dst + d) =
+            f32x4{o[db][4 * q4 + 0], o[db][4 * q4 + 1], o[db][4 * q4 + 2], o[db][4 * q4 + 3]};
+      }
+    if (half == 0) {
+      p.m_part[idx] = m_run;
+      p.l_part[idx] = l_tot;
+    }
+    return;
+  }
   const float inv = 1.0f / l_tot;
   uint16_t* dst = p.out + q_off;
 #pragma unroll
@@ -217,6 +244,42 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
                     pack2_bf16(o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv)};
       *reinterpret_cast<u32x2*>(dst + d) = v;
     }
+}
+
+// Combine the key-split partials of each (block row, query head): one wavefront per pair,
+// splits merged in index order (max, rescale, sum), output rounded to bf16.
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p, int total_block) {
+  const int lane = threadIdx.x & 63;
+  const int rh = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (rh >= total_block * p.hq) return;  // uniform per wavefront
+  const int row = rh / p.hq;
+  // sequence of this row: largest b with cu_block[b] <= row (blocks are non-empty here)
+  int lo = 0, hi = static_cast<int>(gridDim.y) - 1;  // gridDim.y carries the batch size
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.cu_block[mid] <= row) lo = mid; else hi = mid - 1;
+  }
+  const int b = lo;
+  const int n_keys = (p.cu_prefix[b + 1] - p.cu_prefix[b]) + (p.cu_block[b + 1] - p.cu_block[b]);
+  const int nvalid = min(p.nsplit, (n_keys + p.kps - 1) / p.kps);
+  const size_t base = static_cast<size_t>(rh) * p.nsplit;
+  float M = -INFINITY;
+  for (int k = 0; k < nvalid; ++k) M = fmaxf(M, p.m_part[base + k]);
+  constexpr int kPer = D / 64;  // values per lane
+  float acc[kPer] = {};
+  float L = 0.f;
+  for (int k = 0; k < nvalid; ++k) {
+    const float f = fast_exp2(p.m_part[base + k] - M);
+    L += f * p.l_part[base + k];
+    const float* o = p.o_part + (base + k) * D + lane * kPer;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) acc[e] += f * o[e];
+  }
+  const float inv = 1.0f / L;
+  uint16_t* dst = p.out + static_cast<size_t>(rh) * D + lane * kPer;
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) dst[e] = f32_to_bf16_bits_rne(acc[e] * inv);
 }
 
 // fp32 path (small shapes): one wavefront per (block row, query head); lanes split the head
@@ -269,9 +332,37 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParamsF32 p) {
   if (lane + 64 < D) dst[lane + 64] = a1 / l;
 }
 
+// Key-split plan: enough workgroups to fill the chip (kTargetWgs), in whole 64-key stages.
+constexpr int kTargetWgs = 512;
+
+struct SplitPlan {
+  int nsplit, kps;
+};
+
+SplitPlan split_plan(int batch, int max_block, int max_prefix, int hq, int hkv) {
+  const int group = hq / hkv;
+  const long row_tiles = (static_cast<long>(max_block) * group + kRowsPerWg - 1) / kRowsPerWg;
+  const long base = row_tiles * hkv * batch;
+  const int stages = (max_prefix + max_block + kKeys - 1) / kKeys;
+  int nsplit = static_cast<int>((kTargetWgs + base - 1) / base);
+  nsplit = max(1, min(nsplit, stages));
+  const int stages_per = (stages + nsplit - 1) / nsplit;
+  const int kps = stages_per * kKeys;
+  nsplit = (stages * kKeys + kps - 1) / kps;
+  return SplitPlan{nsplit, kps};
+}
+
 }  // namespace
 
-hipError_t block_attn(bool bf16, const AttnArgs& a, hipStream_t s) {
+size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_block, int max_block,
+                           int max_prefix, int hq, int hkv, int head_dim) {
+  if (!bf16 || !allow_split || total_block == 0 || max_block == 0) return 0;
+  const SplitPlan sp = split_plan(batch, max_block, max_prefix, hq, hkv);
+  if (sp.nsplit == 1) return 0;
+  return static_cast<size_t>(total_block) * hq * sp.nsplit * (head_dim + 2) * sizeof(float);
+}
+
+hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s) {
   if (a.total_block == 0 || a.max_block == 0) return hipSuccess;
   const int group = a.hq / a.hkv;
   if (!bf16) {
@@ -282,16 +373,32 @@ hipError_t block_attn(bool bf16, const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(attn_f32_kernel, dim3(a.max_block, a.hq, a.batch), dim3(64), 0, s, p);
     return hipGetLastError();
   }
+  const SplitPlan sp = allow_split ? split_plan(a.batch, a.max_block, a.max_prefix, a.hq, a.hkv)
+                                   : SplitPlan{1, (a.max_prefix + a.max_block + kKeys - 1) / kKeys * kKeys};
+  const size_t n_part = static_cast<size_t>(a.total_block) * a.hq * sp.nsplit;
+  float* o_part = static_cast<float*>(ws);
+  float* m_part = sp.nsplit > 1 ? o_part + n_part * a.head_dim : nullptr;
+  float* l_part = sp.nsplit > 1 ? m_part + n_part : nullptr;
   AttnParams p{a.cu_block, a.cu_prefix, a.hq, a.hkv, group, a.scale * kLog2e,
                static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k_blk),
                static_cast<const uint16_t*>(a.v_blk), static_cast<const uint16_t*>(a.k_pre),
-               static_cast<const uint16_t*>(a.v_pre), static_cast<uint16_t*>(a.out)};
+               static_cast<const uint16_t*>(a.v_pre), static_cast<uint16_t*>(a.out),
+               sp.nsplit, sp.kps, sp.nsplit > 1 ? o_part : nullptr, m_part, l_part};
   const long rows = static_cast<long>(a.max_block) * group;
-  dim3 grid(static_cast<unsigned>((rows + kRowsPerWg - 1) / kRowsPerWg), a.hkv, a.batch);
+  dim3 grid(static_cast<unsigned>((rows + kRowsPerWg - 1) / kRowsPerWg), a.hkv,
+            static_cast<unsigned>(a.batch) * sp.nsplit);
   if (a.head_dim == 128)
     hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kThreads), 0, s, p);
   else
     hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kThreads), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || sp.nsplit == 1) return e;
+  const long pairs = static_cast<long>(a.total_block) * a.hq;
+  dim3 mgrid(static_cast<unsigned>((pairs + 3) / 4), static_cast<unsigned>(a.batch));
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL(attn_merge_kernel<128>, mgrid, dim3(256), 0, s, p, a.total_block);
+  else
+    hipLaunchKernelGGL(attn_merge_kernel<64>, mgrid, dim3(256), 0, s, p, a.total_block);
   return hipGetLastError();
 }
 

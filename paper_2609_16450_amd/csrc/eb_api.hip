@@ -128,20 +128,25 @@ const char* eb_last_error(void) { return g_last_error.c_str(); }
 
 const char* eb_version(void) { return "libeb 0.1 (gfx950)"; }
 
-size_t eb_block_attn_workspace(eb_dtype, const eb_ragged*, int, int, int) { return 0; }
+size_t eb_block_attn_workspace(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim) {
+  if (!r || r->batch < 1 || hq < 1 || hkv < 1 || hq % hkv || r->total_block <= 0) return 0;
+  return round_up(eb::block_attn_ws_bytes(dt == EB_BF16, true, r->batch, r->total_block,
+                                          r->max_block, r->max_prefix, hq, hkv, head_dim));
+}
 
 eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim,
                         float scale, const void* q, const void* k_blk, const void* v_blk,
                         const void* k_pre, const void* v_pre, void* out, void* ws,
                         size_t ws_bytes, eb_stream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   eb_status st = check_attn(dt, r, hq, hkv, head_dim, scale, q, k_blk, v_blk, k_pre, v_pre, out);
   if (st != EB_OK) return st;
+  const size_t need = eb_block_attn_workspace(dt, r, hq, hkv, head_dim);
+  if (ws_bytes < need || (need && !ws))
+    return fail(EB_ERR_WORKSPACE, "attention workspace %zu bytes < required %zu", ws_bytes, need);
   eb::AttnArgs a{r->batch, r->total_block, r->max_block, r->total_prefix, r->max_prefix,
                  r->cu_block, r->cu_prefix, hq, hkv, head_dim, scale, q, k_blk, v_blk,
                  k_pre, v_pre, out};
-  return hip_status(eb::block_attn(dt == EB_BF16, a, stream), "eb_block_attn launch");
+  return hip_status(eb::block_attn(dt == EB_BF16, true, a, ws, stream), "eb_block_attn launch");
 }
 
 size_t eb_lmhead_workspace(eb_dtype dt, int n_rows, int hidden, int vocab) {
@@ -180,7 +185,7 @@ eb_status eb_unmask_select(const eb_ragged* r, const float* conf, const int32_t*
 
 size_t eb_decode_step_workspace(const eb_step_desc* d) {
   if (!d) return 0;
-  return round_up(eb_block_attn_workspace(d->dtype, &d->ragged, d->hq, d->hkv, d->head_dim)) +
+  return eb_block_attn_workspace(d->dtype, &d->ragged, d->hq, d->hkv, d->head_dim) +
          eb_lmhead_workspace(d->dtype, d->ragged.total_block, d->hidden, d->vocab);
 }
 
@@ -210,12 +215,14 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
   eb::AttnArgs a{r->batch, r->total_block, r->max_block, r->total_prefix, r->max_prefix,
                  r->cu_block, r->cu_prefix, d->hq, d->hkv, d->head_dim, scale, d->q, d->k_blk,
                  d->v_blk, d->k_pre, d->v_pre, d->attn_out};
+  const size_t attn_ws = eb_block_attn_workspace(d->dtype, r, d->hq, d->hkv, d->head_dim);
+  char* lm_ws = static_cast<char*>(ws) + attn_ws;
+
   hipError_t e = tr ? mark(tr->attn_begin) : hipSuccess;
-  if (e == hipSuccess) e = eb::block_attn(bf16, a, stream);
+  if (e == hipSuccess) e = eb::block_attn(bf16, true, a, ws, stream);
   if (e == hipSuccess && tr) e = mark(tr->attn_end);
   if (e != hipSuccess) return hip_status(e, "step attention launch");
-  char* lm_ws = static_cast<char*>(ws) +
-                round_up(eb_block_attn_workspace(d->dtype, r, d->hq, d->hkv, d->head_dim));
+
   if (tr) e = mark(tr->lmhead_begin);
   if (e == hipSuccess && T > 0)
     e = eb::lmhead_partials(bf16, T, d->hidden, d->vocab, d->h, d->w, lm_ws, stream);

@@ -43,10 +43,11 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits_rne(float f) {
 //   m = max z,  s = sum 2^((z - m) log2 e),  t = sum 2^((z - m) log2 e) * (z - m) log2 e,
 //   idx = lowest index attaining m.
 // Then kappa = 1 / s and H = ln s - ln2 * t / s.
-struct Partial {
+struct alignas(16) Partial {
   float m, s, t;
   int32_t idx;
 };
+
 
 __device__ __forceinline__ Partial partial_empty() { return Partial{kNegBig, 0.f, 0.f, kNoIndex}; }
 
@@ -81,6 +82,25 @@ __device__ __forceinline__ Partial partial_shfl_xor(const Partial& p, int mask) 
 __device__ __forceinline__ Partial partial_xor_merge(const Partial& p, int mask, int lane) {
   const Partial q = partial_shfl_xor(p, mask);
   return (lane & mask) ? partial_merge(q, p) : partial_merge(p, q);
+}
+
+// Merge of n partials p[0..n) by one wavefront in a fixed order: lane l merges p[l], p[l+64],
+// ... in index order, then a canonical butterfly; every lane ends with the same result.  Loads
+// are issued kBatch at a time, unconditionally (clamped index, masked merge), so that their
+// latencies overlap.
+template <int kBatch = 4>
+__device__ __forceinline__ Partial wave_merge(const Partial* __restrict__ p, int n, int lane) {
+  Partial acc = partial_empty();
+  for (int base = 0; base < n; base += 64 * kBatch) {  // uniform trip count
+    Partial q[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) q[j] = p[min(base + 64 * j + lane, n - 1)];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+      if (base + 64 * j + lane < n) acc = partial_merge(acc, q[j]);
+  }
+  for (int mask = 32; mask >= 1; mask >>= 1) acc = partial_xor_merge(acc, mask, lane);
+  return acc;
 }
 
 }  // namespace eb

@@ -28,7 +28,11 @@ struct AttnArgs {
   const void *q, *k_blk, *v_blk, *k_pre, *v_pre;
   void* out;
 };
-hipError_t block_attn(bool bf16, const AttnArgs& a, hipStream_t s);
+// Workspace for key-split partials (0 when the launch needs no split).  Without allow_split
+// one workgroup covers all keys of its query tile and no workspace is used.
+size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_block,
+                           int max_block, int max_prefix, int hq, int hkv, int head_dim);
+hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s);
 
 // ---- unmask ---------------------------------------------------------------------------
 hipError_t unmask_select(int batch, int max_block, const int32_t* cu_block, const float* conf,

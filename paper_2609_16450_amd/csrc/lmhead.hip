@@ -730,10 +730,7 @@ __global__ __launch_bounds__(256) void lmhead_combine_kernel(const Partial* __re
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n_rows) return;  // uniform per wavefront
-  const Partial* pr = part + static_cast<size_t>(row) * n_slices;
-  Partial p = partial_empty();
-  for (int i = lane; i < n_slices; i += 64) p = partial_merge(p, pr[i]);
-  for (int mask = 32; mask >= 1; mask >>= 1) p = partial_xor_merge(p, mask, lane);
+  const Partial p = wave_merge(part + static_cast<size_t>(row) * n_slices, n_slices, lane);
   if (lane == 0) {
     conf[row] = 1.0f / p.s;
     entropy[row] = logf(p.s) - kLn2 * p.t / p.s;

@@ -23,14 +23,15 @@ __device__ __forceinline__ Best best_of(Best a, Best b) {
   return a.i <= b.i ? a : b;
 }
 
-__global__ __launch_bounds__(kThreads) void unmask_kernel(
-    const int32_t* __restrict__ cu_block, const float* __restrict__ conf,
+// Unmask of block b by one workgroup of kThreads threads.
+__device__ __forceinline__ void unmask_block(
+    int b, const int32_t* __restrict__ cu_block, const float* __restrict__ conf,
     const int32_t* __restrict__ argmax, const float* __restrict__ tau,
-    uint8_t* __restrict__ masked, int32_t* __restrict__ tokens, uint8_t* __restrict__ unmask,
-    int32_t* __restrict__ n_commit, uint8_t* __restrict__ resolved) {
+    uint8_t* __restrict__ masked,
+    int32_t* __restrict__ tokens, uint8_t* __restrict__ unmask, int32_t* __restrict__ n_commit,
+    uint8_t* __restrict__ resolved) {
   __shared__ int s_pass[kThreads / 64], s_masked[kThreads / 64];
   __shared__ Best s_best[kThreads / 64];
-  const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int beg = cu_block[b], end = cu_block[b + 1];
   const float tb = tau[b];
@@ -81,6 +82,15 @@ __global__ __launch_bounds__(kThreads) void unmask_kernel(
     n_commit[b] = commits;
     resolved[b] = (n_masked - commits == 0) ? 1 : 0;
   }
+}
+
+__global__ __launch_bounds__(kThreads) void unmask_kernel(
+    const int32_t* __restrict__ cu_block, const float* __restrict__ conf,
+    const int32_t* __restrict__ argmax, const float* __restrict__ tau,
+    uint8_t* __restrict__ masked, int32_t* __restrict__ tokens, uint8_t* __restrict__ unmask,
+    int32_t* __restrict__ n_commit, uint8_t* __restrict__ resolved) {
+  unmask_block(blockIdx.x, cu_block, conf, argmax, tau, masked, tokens, unmask, n_commit,
+               resolved);
 }
 
 }  // namespace
