@@ -661,13 +661,181 @@ __global__ __launch_bounds__(128 * WN, MINB) void lmhead_tile_kernel(
   }
 }
 
-// Tile shape of the large-batch path.  Variant 2 (default): 256 x 256 tiles, 8 waves, ring of 4
-// (128 KB LDS, one workgroup per compute unit).  Variant 1: 256 x 128 tiles, 4 waves, ring of 3
-// (72 KB, two workgroups per compute unit); measured 10% slower at batch 64.
+#ifndef EB_TILE4_SCHED
+#define EB_TILE4_SCHED 1
+#endif
+
+// Wait until at most N vector-memory instructions of this wave are outstanding and all of its
+// LDS reads have returned, then barrier.
+template <int N>
+__device__ __forceinline__ void wait_vm_lds_and_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0x0 << 8));
+  asm volatile("s_barrier" ::: "memory");
+}
+
+// 256 x 256 tiles computed by 4 waves as a 2 x 2 grid of 128 x 128 sub-tiles (4 x 4 blocks of
+// 32x32x16 MFMAs, 256 accumulator registers per lane).  Per 32-column k step a wave reads
+// 16 KB of operand fragments from LDS (the 8-wave 128 x 64 split reads 12 KB per wave, 96 KB
+// per tile against 64 KB here).  The fragments of the two 16-column halves of a k step are
+// double-buffered in registers: the reads of one half are issued before the MFMAs of the
+// other, so LDS latency hides under 16 MFMAs.  The DMA ring keeps RING stages occupied: right
+// after the barrier that ends the reads of stage kt, stage kt + RING is issued into its slot.
+template <int RING>
+__global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
+    const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
+    int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part) {
+  constexpr int BM = kTileBM, BN = 256, BK = kTileBK;
+  constexpr int WM = 2, WN = 2, kWaves = WM * WN;
+  constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
+  constexpr int TM = kWaveM / 32, TN = kWaveN / 32;
+  constexpr int kRowB = BK * 2;                   // 64 bytes per LDS row
+  constexpr int kStageBytes = (BM + BN) * kRowB;  // 32 KB
+  constexpr int kInst = (BM + BN) / 16;           // 1 KB wave instructions per stage
+  constexpr int kInstPerWave = kInst / kWaves;    // 8
+  static_assert(RING >= 2 && RING <= 4, "ring of 2 to 4 stages");
+  static_assert((RING - 1) * kInstPerWave < 64, "vmcnt range");
+  __shared__ __attribute__((aligned(16))) uint8_t smem[RING * kStageBytes];
+  static_assert(WM * BN * sizeof(Partial) <= RING * kStageBytes, "reduction fits in the ring");
+
+  const int id = blockIdx.x;
+  const int xcd = id % kXcds, k = id / kXcds;
+  const int per_band = kBand * n_rtiles;
+  const int band = xcd + kXcds * (k / per_band);
+  if (band >= n_bands) return;
+  const int tt = k % per_band;
+  const int nv = min(kBand, n_vtiles - band * kBand);
+  if (tt >= nv * n_rtiles) return;
+  const int vt = band * kBand + tt % nv;
+  const int rt = tt / nv;
+  const int v0 = vt * BM, r0 = rt * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int half = lane >> 5, l32 = lane & 31;
+
+  // Load instruction i of this wave covers tile rows 16 q .. 16 q + 15, q = wave * 8 + i (rows
+  // below BM are W, the rest h); lane L fetches row 16 q + L / 4, global chunk
+  // (L % 4) ^ swizzle(row) into LDS slot L % 4 of the row.  Rows past the end are clamped.
+  const uint16_t* src[kInstPerWave];
+#pragma unroll
+  for (int i = 0; i < kInstPerWave; ++i) {
+    const int q = wave * kInstPerWave + i;
+    const int row = 16 * q + (lane >> 2);
+    const int chunk = (lane & 3) ^ ((row >> 2) & 3);
+    src[i] = row < BM
+                 ? w + static_cast<size_t>(min(v0 + row, vocab - 1)) * hidden + chunk * 8
+                 : h + static_cast<size_t>(min(r0 + row - BM, n_rows - 1)) * hidden + chunk * 8;
+  }
+  // Stage `stage` of the k loop into ring slot `slot`.
+  auto issue = [&](int stage, int slot) {
+    uint8_t* base = smem + slot * kStageBytes;
+#pragma unroll
+    for (int i = 0; i < kInstPerWave; ++i)
+      load_to_lds(src[i] + stage * BK, base + (wave * kInstPerWave + i) * 1024);
+  };
+  // Fragments of half s (k columns 16 s .. 16 s + 15 of the stage, chunk 2 half + s per lane).
+  auto read = [&](int kt, int s, bf16x8 (&a)[TM], bf16x8 (&b)[TN]) {
+    const uint8_t* st = smem + (kt % RING) * kStageBytes;
+    const int c = 2 * half + s;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      const int r = wm * kWaveM + tm * 32 + l32;
+      a[tm] = *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (c ^ ((r >> 2) & 3)));
+    }
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int r = BM + wn * kWaveN + tn * 32 + l32;
+      b[tn] = *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (c ^ ((r >> 2) & 3)));
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b) acc[a][b] = f32x16{};
+  auto mma = [&](const bf16x8 (&a)[TM], const bf16x8 (&b)[TN]) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32(a[tm], b[tn], acc[tm][tn]);
+  };
+  // Every iteration issues exactly one stage (past the end: the last stage again, into the slot
+  // just freed, never read), so the number of younger stages in flight at each barrier is
+  // always RING - 2 and every wait is the same; straight-line code lets the fragment reads of
+  // one half stay in flight under the MFMAs of the other.
+  const int nk = hidden / BK;  // >= 1
+#pragma unroll
+  for (int j = 0; j < RING; ++j) issue(min(j, nk - 1), j);
+  wait_vm_lds_and_barrier<(RING - 1) * kInstPerWave>();
+  bf16x8 xa[TM], xb[TN], ya[TM], yb[TN];
+  read(0, 0, xa, xb);
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    read(kt, 1, ya, yb);
+    mma(xa, xb);
+#if EB_TILE4_SCHED
+    // one fragment read after each of the first 8 MFMAs
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+#endif
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm_lds_and_barrier<(RING - 2) * kInstPerWave>();  // stage kt + 1 has landed
+    issue(min(kt + RING, nk - 1), kt % RING);               // slot of stage kt, fully read
+    read(kt + 1, 0, xa, xb);
+    mma(ya, yb);
+#if EB_TILE4_SCHED
+    // one DMA load after each of the first 8 MFMAs, one fragment read after each of the rest
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+#endif
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  read(nk - 1, 1, ya, yb);
+  mma(xa, xb);
+  mma(ya, yb);
+  wait_vm_lds_and_barrier<0>();  // no DMA in flight; every wave is done reading the ring
+
+  Partial* red = reinterpret_cast<Partial*>(smem);  // [WM][BN]
+  const bool full = v0 + BM <= vocab;
+  const int vbase = v0 + wm * kWaveM + 4 * half;
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    Partial p = column_partial<TM, TN>(acc, tn, vbase, vocab, full);
+    p = partial_xor_merge(p, 32, lane);
+    if (lane < 32) red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
+  }
+  __syncthreads();
+  for (int c = tid; c < BN; c += kWaves * 64) {
+    Partial p = red[c];
+#pragma unroll
+    for (int q = 1; q < WM; ++q) p = partial_merge(p, red[q * BN + c]);
+    const int row = r0 + c;
+    if (row < n_rows) part[static_cast<size_t>(row) * n_vtiles + vt] = p;
+  }
+}
+
+// Tile kernel of the large-batch path.  Variant 5 (default): lmhead_tile4_kernel, 256 x 256
+// tiles, 4 waves of 128 x 128, ring of 4 (128 KB LDS, one workgroup per compute unit); batch 64:
+// 9.82 ms.  Variant 2: lmhead_tile_kernel with 8 waves of 128 x 64; 10.55 ms.  Variant 1:
+// 256 x 128 tiles, 4 waves, ring of 3 (72 KB, two workgroups per compute unit); 11.8 ms.
 #ifndef EB_TILE_VARIANT
-#define EB_TILE_VARIANT 2
+#define EB_TILE_VARIANT 5
 #endif
 constexpr int kTileBN = EB_TILE_VARIANT == 1 ? 128 : 256;
+static_assert(EB_TILE_VARIANT == 1 || EB_TILE_VARIANT == 2 || EB_TILE_VARIANT == 5, "tile variant");
 
 hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const void* w,
                        Partial* part, hipStream_t s) {
@@ -677,6 +845,9 @@ hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const v
   if constexpr (EB_TILE_VARIANT == 1) {
     hipLaunchKernelGGL((lmhead_tile_kernel<2, 128, 3, 2>), dim3(m.grid), dim3(256), 0, s, hp, wp,
                        n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
+  } else if constexpr (EB_TILE_VARIANT == 5) {
+    hipLaunchKernelGGL((lmhead_tile4_kernel<4>), dim3(m.grid), dim3(256), 0, s, hp, wp, n_rows,
+                       hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
   } else {
     hipLaunchKernelGGL((lmhead_tile_kernel<4, 256, 4, 1>), dim3(m.grid), dim3(512), 0, s, hp, wp,
                        n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
