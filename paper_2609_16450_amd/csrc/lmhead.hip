@@ -513,21 +513,24 @@ __device__ __forceinline__ void wait_stage(int later) {
 }
 
 // Partial statistics of one lane's column over TM 32-row MFMA blocks.  Element (tm, r) of the
-// lane is vocabulary row vbase + 32 tm + 8 (r / 4) + (r % 4).  The max comes first; the exp pass
-// then walks the rows in decreasing order, so the last z == max hit is the lowest row.
+// lane is vocabulary row vbase + 32 tm + 8 (r / 4) + (r % 4).  Four independent chains (by
+// r % 4) carry the max, the sums and the first argmax, so the reduction is not bound by the
+// latency of one long dependency chain; each chain walks its rows in decreasing order, so its
+// last z == max hit is its lowest row, and the chains are combined at the end.
 template <int TM, int TN>
 __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], int tn, int vbase,
                                                   int vocab, bool full) {
-  float m = kNegBig;
+  float mc[4] = {kNegBig, kNegBig, kNegBig, kNegBig};
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int v = vbase + tm * 32 + 8 * (r >> 2) + (r & 3);
-      if (full || v < vocab) m = fmaxf(m, acc[tm][tn][r]);
+      if (full || v < vocab) mc[r & 3] = fmaxf(mc[r & 3], acc[tm][tn][r]);
     }
-  float s = 0.f, t = 0.f;
-  int32_t idx = kNoIndex;
+  const float m = fmaxf(fmaxf(mc[0], mc[1]), fmaxf(mc[2], mc[3]));
+  float sc[4] = {0.f, 0.f, 0.f, 0.f}, tc[4] = {0.f, 0.f, 0.f, 0.f};
+  int32_t ic[4] = {kNoIndex, kNoIndex, kNoIndex, kNoIndex};
 #pragma unroll
   for (int tm = TM - 1; tm >= 0; --tm)
 #pragma unroll
@@ -539,11 +542,12 @@ __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], i
       // m = kNegBig, where z - m would overflow and 0 * inf would poison t)
       const float y = ok ? (z - m) * kLog2e : 0.f;
       const float e = ok ? fast_exp2(y) : 0.f;
-      s += e;
-      t = fmaf(e, y, t);
-      idx = (ok && z == m) ? v : idx;
+      sc[r & 3] += e;
+      tc[r & 3] = fmaf(e, y, tc[r & 3]);
+      ic[r & 3] = (ok && z == m) ? v : ic[r & 3];
     }
-  return Partial{m, s, t, idx};
+  return Partial{m, (sc[0] + sc[1]) + (sc[2] + sc[3]), (tc[0] + tc[1]) + (tc[2] + tc[3]),
+                 min(min(ic[0], ic[1]), min(ic[2], ic[3]))};
 }
 
 template <int WN, int BN, int RING, int MINB>
@@ -661,10 +665,6 @@ __global__ __launch_bounds__(128 * WN, MINB) void lmhead_tile_kernel(
   }
 }
 
-#ifndef EB_TILE4_SCHED
-#define EB_TILE4_SCHED 1
-#endif
-
 // Wait until at most N vector-memory instructions of this wave are outstanding and all of its
 // LDS reads have returned, then barrier.
 template <int N>
@@ -774,7 +774,6 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
   for (int kt = 0; kt + 1 < nk; ++kt) {
     read(kt, 1, ya, yb);
     mma(xa, xb);
-#if EB_TILE4_SCHED
     // one fragment read after each of the first 8 MFMAs
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -782,25 +781,22 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-#endif
     __builtin_amdgcn_sched_barrier(0);
     wait_vm_lds_and_barrier<(RING - 2) * kInstPerWave>();  // stage kt + 1 has landed
     issue(min(kt + RING, nk - 1), kt % RING);               // slot of stage kt, fully read
     read(kt + 1, 0, xa, xb);
     mma(ya, yb);
-#if EB_TILE4_SCHED
     // one DMA load after each of the first 8 MFMAs, one fragment read after each of the rest
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-#endif
     __builtin_amdgcn_sched_barrier(0);
   }
   read(nk - 1, 1, ya, yb);
@@ -829,13 +825,18 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
 
 // Tile kernel of the large-batch path.  Variant 5 (default): lmhead_tile4_kernel, 256 x 256
 // tiles, 4 waves of 128 x 128, ring of 4 (128 KB LDS, one workgroup per compute unit); batch 64:
-// 9.82 ms.  Variant 2: lmhead_tile_kernel with 8 waves of 128 x 64; 10.55 ms.  Variant 1:
+// 9.6 ms.  Variant 2: lmhead_tile_kernel with 8 waves of 128 x 64; 10.55 ms.  Variant 1:
 // 256 x 128 tiles, 4 waves, ring of 3 (72 KB, two workgroups per compute unit); 11.8 ms.
+// Measured and dropped: stages reaching LDS through registers (9.65 ms), 64-column stages with
+// one barrier per 64 MFMAs (10.1 ms), DMA loads spread over both halves of a step (no change);
+// with every operand L2-resident the kernel runs at the same speed, so it is bound by the
+// issue/LDS schedule of one wave per SIMD, not by memory.
 #ifndef EB_TILE_VARIANT
 #define EB_TILE_VARIANT 5
 #endif
 constexpr int kTileBN = EB_TILE_VARIANT == 1 ? 128 : 256;
-static_assert(EB_TILE_VARIANT == 1 || EB_TILE_VARIANT == 2 || EB_TILE_VARIANT == 5, "tile variant");
+static_assert(EB_TILE_VARIANT == 1 || EB_TILE_VARIANT == 2 || EB_TILE_VARIANT == 5,
+              "tile variant");
 
 hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const void* w,
                        Partial* part, hipStream_t s) {
