@@ -53,6 +53,14 @@ def lmhead_work(cfg, T: int):
     return nbytes, flops
 
 
+def lmhead_kernel_name(dtype: str, T: int) -> str:
+    """The LM-head kernel the library launches for T rows (the streaming kernel for at most 64
+    bf16 rows, the tile kernel above)."""
+    if dtype == "f32":
+        return "lmhead_f32_kernel"
+    return "lmhead_stream16_kernel" if T <= 64 else "lmhead_tile4_kernel"
+
+
 def measured_traffic(workload: str):
     """HBM bytes per launch from rocprofv3 counters, if taken on the current kernel source."""
     try:
@@ -207,7 +215,7 @@ def main() -> int:
                    "ms_per_step_events": ms_events},
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": measured_traffic(cfg.name),
-                     "kernel": "lmhead_bf16_kernel" if cfg.dtype == "bf16" else "lmhead_f32_kernel",
+                     "kernel": lmhead_kernel_name(cfg.dtype, T),
                      "kernel_us": lm_ms * 1e3, "algorithmic_bytes": nbytes,
                      "algorithmic_flops": flops},
     }

@@ -25,7 +25,10 @@ namespace {
 // ---------------------------------------------------------------------------------------
 constexpr int kStreamWaves = 8;
 constexpr int kStreamThreads = kStreamWaves * 64;
-constexpr int kStreamGroups = 256;  // workgroups (one per MI355X compute unit)
+#ifndef EB_STREAM_GROUPS
+#define EB_STREAM_GROUPS 256
+#endif
+constexpr int kStreamGroups = EB_STREAM_GROUPS;  // workgroups (256: one per compute unit)
 
 template <int TM, int NT, int kDepth>
 __global__ __launch_bounds__(kStreamThreads) void lmhead_stream_kernel(
