@@ -3,8 +3,10 @@
 TEST INFRASTRUCTURE ONLY: imported by the test suite, the package smoke check
 and the benchmark's CPU-baseline leg, never by the HIP product path."""
 from .eb_oracle import (block_attention, lmhead_logits, confidence_stats, lmhead_confidence,
-                        unmask_select, decode_step)
+                        unmask_select, decode_step, lps_features, unmask_select_lps,
+                        unmask_select_topm, lbs_select)
 from . import margins
 
 __all__ = ["block_attention", "lmhead_logits", "confidence_stats", "lmhead_confidence",
-           "unmask_select", "decode_step", "margins"]
+           "unmask_select", "decode_step", "lps_features", "unmask_select_lps",
+           "unmask_select_topm", "lbs_select", "margins"]
