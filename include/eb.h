@@ -140,6 +140,70 @@ eb_status eb_unmask_select(const eb_ragged* r, const float* conf, const int32_t*
                            int32_t* n_commit, uint8_t* resolved, eb_stream_t stream);
 
 /* ---------------------------------------------------------------------------------------
+ * LM head with the LPS gap feature (Sec. 5.2, Alg. 5): everything eb_lmhead_confidence
+ * computes, plus the gap between the two largest probabilities of each row
+ *
+ *   top2_gap[i] = p_(1) - p_(2)    (p sorted in decreasing order, counted with multiplicity:
+ *                                   0 when the largest logit is shared; p_(2) = 0 if vocab = 1)
+ *
+ * computed as (1 - exp(z_(2) - z_(1))) / sum_v exp(z_v - z_(1)) from the two largest logits,
+ * which the kernels track next to the row maximum.  Same requirements as eb_lmhead_confidence;
+ * top2_gap [n_rows] f32 is required.  ws: at least eb_lmhead_features_workspace(...) bytes.
+ * ------------------------------------------------------------------------------------- */
+size_t eb_lmhead_features_workspace(eb_dtype dt, int n_rows, int hidden, int vocab);
+eb_status eb_lmhead_features(eb_dtype dt, int n_rows, int hidden, int vocab, const void* h,
+                             const void* w, float* conf, float* entropy_nats, int32_t* argmax,
+                             float* max_logit, float* top2_gap, void* ws, size_t ws_bytes,
+                             eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * LPS router inputs of every block row (Sec. 5.2; Alg. 5, feature tuple and intra-block
+ * position).  For row i of block b (rows cu_block[b] .. cu_block[b+1]-1, len_b rows):
+ *
+ *   rho_b      = (masked rows of block b) / len_b     (block-wise mask ratio before commit)
+ *   feat[i]    = (conf[i], entropy_nats[i] / ln(vocab), top2_gap[i], rho_b)   [T, 4] f32
+ *   pos[i]     = (i - cu_block[b]) / len_b            [T] f32 (rank within the packed block)
+ *   mask_ratio[b] = rho_b                             [B] f32, optional (NULL to skip)
+ *
+ * The router itself is not part of this library: its commit probability p_psi comes back
+ * through eb_unmask_select_lps.  Requires vocab >= 2 and feat 16-byte aligned; only r->batch,
+ * r->total_block and r->cu_block are used.
+ * ------------------------------------------------------------------------------------- */
+eb_status eb_lps_features(const eb_ragged* r, int vocab, const float* conf,
+                          const float* entropy_nats, const float* top2_gap,
+                          const uint8_t* masked, float* feat, float* pos, float* mask_ratio,
+                          eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Union accept rule of Alg. 5 (Sec. 5.2, LPS router inference): as eb_unmask_select, with
+ *
+ *   A_b = { i : masked[i] && (conf[i] >= tau[b] || p_psi[i] > tau_psi) }
+ *
+ * and the same anti-stall fallback and commit.  p_psi [T] f32 is the caller's router commit
+ * probability per block row (rows that are not masked are ignored).
+ * ------------------------------------------------------------------------------------- */
+eb_status eb_unmask_select_lps(const eb_ragged* r, const float* conf, const int32_t* argmax,
+                               const float* tau, const float* p_psi, float tau_psi,
+                               uint8_t* masked, int32_t* tokens, uint8_t* unmask,
+                               int32_t* n_commit, uint8_t* resolved, eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Budgeted block update (Eq. prelim-update with a per-step budget m): as eb_unmask_select,
+ * with
+ *
+ *   A_b = { i : masked[i] && conf[i] >= tau[b] }  united with
+ *         Top-m_b = the m masked rows of block b with the largest conf (equal conf: the lower
+ *                   row first; every masked row if fewer than m)
+ *
+ * m = 0 gives the threshold rule with its anti-stall fallback; a tau above 1 disables the
+ * threshold.  Requires m >= 0.
+ * ------------------------------------------------------------------------------------- */
+eb_status eb_unmask_select_topm(const eb_ragged* r, const float* conf, const int32_t* argmax,
+                                const float* tau, int32_t m, uint8_t* masked, int32_t* tokens,
+                                uint8_t* unmask, int32_t* n_commit, uint8_t* resolved,
+                                eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
  * One whole denoising step: eb_block_attn, then eb_lmhead_confidence over the T block rows
  * of h, then eb_unmask_select, enqueued on `stream` with no host synchronisation.  The
  * workspace holds the attention's key-split partials followed by the LM-head partials.

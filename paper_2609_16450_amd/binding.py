@@ -60,6 +60,16 @@ EXPORTS = {
                                             ctypes.c_size_t, _P]),
     "eb_unmask_select": (ctypes.c_int, [ctypes.POINTER(eb_ragged), _P, _P, _P, _P, _P, _P, _P,
                                         _P, _P]),
+    "eb_lmhead_features_workspace": (ctypes.c_size_t, [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                       ctypes.c_int]),
+    "eb_lmhead_features": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                          _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "eb_lps_features": (ctypes.c_int, [ctypes.POINTER(eb_ragged), ctypes.c_int, _P, _P, _P, _P,
+                                       _P, _P, _P, _P]),
+    "eb_unmask_select_lps": (ctypes.c_int, [ctypes.POINTER(eb_ragged), _P, _P, _P, _P,
+                                            ctypes.c_float, _P, _P, _P, _P, _P, _P]),
+    "eb_unmask_select_topm": (ctypes.c_int, [ctypes.POINTER(eb_ragged), _P, _P, _P,
+                                             ctypes.c_int32, _P, _P, _P, _P, _P, _P]),
     "eb_decode_step_workspace": (ctypes.c_size_t, [ctypes.POINTER(eb_step_desc)]),
     "eb_decode_step": (ctypes.c_int, [ctypes.POINTER(eb_step_desc), _P, ctypes.c_size_t, _P]),
     "eb_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -271,6 +281,88 @@ def eb_unmask_select(r: Ragged, conf, argmax, tau, masked, tokens, unmask, n_com
                                    unmask.data_ptr(), n_commit.data_ptr(), resolved.data_ptr(),
                                    _stream(stream)),
            "eb_unmask_select")
+
+
+def eb_lmhead_features_workspace(dtype: int, n_rows: int, hidden: int, vocab: int) -> int:
+    return int(load().eb_lmhead_features_workspace(dtype, n_rows, hidden, vocab))
+
+
+def eb_lmhead_features(h, w, conf, entropy_nats, argmax, top2_gap, max_logit=None,
+                       ws: Optional[torch.Tensor] = None, stream=None) -> None:
+    """eb_lmhead_confidence plus the top-1/top-2 probability gap per row (eb.h)."""
+    dt = _dtype_code(h)
+    n_rows, hidden = h.shape
+    vocab = w.shape[0]
+    _dev(h, "h", h.dtype, (n_rows, hidden))
+    _dev(w, "w", h.dtype, (vocab, hidden))
+    for name, t, dtype in (("conf", conf, torch.float32), ("entropy_nats", entropy_nats, torch.float32),
+                           ("argmax", argmax, torch.int32), ("top2_gap", top2_gap, torch.float32)):
+        _dev(t, name, dtype, (n_rows,))
+    if max_logit is not None:
+        _dev(max_logit, "max_logit", torch.float32, (n_rows,))
+    lib = load()
+    need = int(lib.eb_lmhead_features_workspace(dt, n_rows, hidden, vocab))
+    wp, wn = _workspace(need, ws, h.device)
+    _check(lib.eb_lmhead_features(dt, n_rows, hidden, vocab, h.data_ptr(), w.data_ptr(),
+                                  conf.data_ptr(), entropy_nats.data_ptr(), argmax.data_ptr(),
+                                  _ptr(max_logit), top2_gap.data_ptr(), wp, wn, _stream(stream)),
+           "eb_lmhead_features")
+
+
+def eb_lps_features(r: Ragged, vocab: int, conf, entropy_nats, top2_gap, masked, feat, pos,
+                    mask_ratio=None, stream=None) -> None:
+    """LPS router inputs feat [T, 4] and intra-block positions pos [T] (eb.h)."""
+    T, B = r.total_block, r.batch
+    for name, t in (("conf", conf), ("entropy_nats", entropy_nats), ("top2_gap", top2_gap),
+                    ("pos", pos)):
+        _dev(t, name, torch.float32, (T,))
+    _dev(masked, "masked", torch.uint8, (T,))
+    _dev(feat, "feat", torch.float32, (T, 4))
+    if mask_ratio is not None:
+        _dev(mask_ratio, "mask_ratio", torch.float32, (B,))
+    rc = r.c()
+    _check(load().eb_lps_features(ctypes.byref(rc), int(vocab), conf.data_ptr(),
+                                  entropy_nats.data_ptr(), top2_gap.data_ptr(), masked.data_ptr(),
+                                  feat.data_ptr(), pos.data_ptr(), _ptr(mask_ratio),
+                                  _stream(stream)),
+           "eb_lps_features")
+
+
+def _unmask_tensors(r: Ragged, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved):
+    T, B = r.total_block, r.batch
+    _dev(conf, "conf", torch.float32, (T,))
+    _dev(argmax, "argmax", torch.int32, (T,))
+    _dev(tau, "tau", torch.float32, (B,))
+    _dev(masked, "masked", torch.uint8, (T,))
+    _dev(tokens, "tokens", torch.int32, (T,))
+    _dev(unmask, "unmask", torch.uint8, (T,))
+    _dev(n_commit, "n_commit", torch.int32, (B,))
+    _dev(resolved, "resolved", torch.uint8, (B,))
+
+
+def eb_unmask_select_lps(r: Ragged, conf, argmax, tau, p_psi, tau_psi: float, masked, tokens,
+                         unmask, n_commit, resolved, stream=None) -> None:
+    """Union accept rule conf >= tau or p_psi > tau_psi, with the anti-stall fallback (eb.h)."""
+    _unmask_tensors(r, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved)
+    _dev(p_psi, "p_psi", torch.float32, (r.total_block,))
+    rc = r.c()
+    _check(load().eb_unmask_select_lps(ctypes.byref(rc), conf.data_ptr(), argmax.data_ptr(),
+                                       tau.data_ptr(), p_psi.data_ptr(), float(tau_psi),
+                                       masked.data_ptr(), tokens.data_ptr(), unmask.data_ptr(),
+                                       n_commit.data_ptr(), resolved.data_ptr(), _stream(stream)),
+           "eb_unmask_select_lps")
+
+
+def eb_unmask_select_topm(r: Ragged, conf, argmax, tau, m: int, masked, tokens, unmask,
+                          n_commit, resolved, stream=None) -> None:
+    """Threshold set united with the m most confident masked rows of each block (eb.h)."""
+    _unmask_tensors(r, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved)
+    rc = r.c()
+    _check(load().eb_unmask_select_topm(ctypes.byref(rc), conf.data_ptr(), argmax.data_ptr(),
+                                        tau.data_ptr(), int(m), masked.data_ptr(),
+                                        tokens.data_ptr(), unmask.data_ptr(), n_commit.data_ptr(),
+                                        resolved.data_ptr(), _stream(stream)),
+           "eb_unmask_select_topm")
 
 
 class StepBuffers:

@@ -152,25 +152,93 @@ eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int he
 size_t eb_lmhead_workspace(eb_dtype dt, int n_rows, int hidden, int vocab) {
   (void)hidden;
   if (n_rows <= 0 || vocab <= 0) return 0;
-  return round_up(eb::lmhead_ws_bytes(dt == EB_BF16, n_rows, vocab));
+  return round_up(eb::lmhead_ws_bytes(dt == EB_BF16, n_rows, vocab, false));
 }
+
+size_t eb_lmhead_features_workspace(eb_dtype dt, int n_rows, int hidden, int vocab) {
+  (void)hidden;
+  if (n_rows <= 0 || vocab <= 0) return 0;
+  return round_up(eb::lmhead_ws_bytes(dt == EB_BF16, n_rows, vocab, true));
+}
+
+namespace {
+eb_status lmhead_run(eb_dtype dt, int n_rows, int hidden, int vocab, const void* h,
+                     const void* w, float* conf, float* entropy_nats, int32_t* argmax,
+                     float* max_logit, float* top2_gap, void* ws, size_t ws_bytes,
+                     eb_stream_t stream) {
+  eb_status st = check_lmhead(dt, n_rows, hidden, vocab, h, w, conf, entropy_nats, argmax);
+  if (st != EB_OK) return st;
+  const bool top2 = top2_gap != nullptr;
+  const size_t need = top2 ? eb_lmhead_features_workspace(dt, n_rows, hidden, vocab)
+                           : eb_lmhead_workspace(dt, n_rows, hidden, vocab);
+  if (ws_bytes < need || (need && !ws))
+    return fail(EB_ERR_WORKSPACE, "LM-head workspace %zu bytes < required %zu", ws_bytes, need);
+  if (n_rows == 0) return ok();
+  const bool bf16 = dt == EB_BF16;
+  hipError_t e = eb::lmhead_partials(bf16, n_rows, hidden, vocab, h, w, ws, top2, stream);
+  if (e != hipSuccess) return hip_status(e, "LM-head partial launch");
+  e = eb::lmhead_combine(bf16, n_rows, vocab, ws, conf, entropy_nats, argmax, max_logit,
+                         top2_gap, stream);
+  return hip_status(e, "LM-head combine launch");
+}
+}  // namespace
 
 eb_status eb_lmhead_confidence(eb_dtype dt, int n_rows, int hidden, int vocab, const void* h,
                                const void* w, float* conf, float* entropy_nats,
                                int32_t* argmax, float* max_logit, void* ws, size_t ws_bytes,
                                eb_stream_t stream) {
-  eb_status st = check_lmhead(dt, n_rows, hidden, vocab, h, w, conf, entropy_nats, argmax);
+  return lmhead_run(dt, n_rows, hidden, vocab, h, w, conf, entropy_nats, argmax, max_logit,
+                    nullptr, ws, ws_bytes, stream);
+}
+
+eb_status eb_lmhead_features(eb_dtype dt, int n_rows, int hidden, int vocab, const void* h,
+                             const void* w, float* conf, float* entropy_nats, int32_t* argmax,
+                             float* max_logit, float* top2_gap, void* ws, size_t ws_bytes,
+                             eb_stream_t stream) {
+  if (n_rows > 0 && !top2_gap) return fail(EB_ERR_INVALID, "NULL top2_gap");
+  return lmhead_run(dt, n_rows, hidden, vocab, h, w, conf, entropy_nats, argmax, max_logit,
+                    top2_gap, ws, ws_bytes, stream);
+}
+
+eb_status eb_lps_features(const eb_ragged* r, int vocab, const float* conf,
+                          const float* entropy_nats, const float* top2_gap,
+                          const uint8_t* masked, float* feat, float* pos, float* mask_ratio,
+                          eb_stream_t stream) {
+  eb_status st = check_ragged(r, false);
   if (st != EB_OK) return st;
-  const size_t need = eb_lmhead_workspace(dt, n_rows, hidden, vocab);
-  if (ws_bytes < need || (need && !ws))
-    return fail(EB_ERR_WORKSPACE, "LM-head workspace %zu bytes < required %zu", ws_bytes, need);
-  if (n_rows == 0) return ok();
-  const bool bf16 = dt == EB_BF16;
-  hipError_t e = eb::lmhead_partials(bf16, n_rows, hidden, vocab, h, w, ws, stream);
-  if (e != hipSuccess) return hip_status(e, "LM-head partial launch");
-  e = eb::lmhead_combine(n_rows, eb::lmhead_num_slices(bf16, n_rows, vocab), ws, conf,
-                         entropy_nats, argmax, max_logit, stream);
-  return hip_status(e, "LM-head combine launch");
+  if (vocab < 2) return fail(EB_ERR_INVALID, "vocab must be >= 2 (got %d)", vocab);
+  if (r->total_block > 0 && (!conf || !entropy_nats || !top2_gap || !masked || !feat || !pos))
+    return fail(EB_ERR_INVALID, "NULL conf / entropy / top2_gap / masked / feat / pos");
+  if (r->total_block > 0 && !aligned16(feat))
+    return fail(EB_ERR_INVALID, "feat must be 16-byte aligned");
+  return hip_status(eb::lps_features(r->batch, r->cu_block, vocab, conf, entropy_nats, top2_gap,
+                                     masked, feat, pos, mask_ratio, stream),
+                    "eb_lps_features launch");
+}
+
+eb_status eb_unmask_select_lps(const eb_ragged* r, const float* conf, const int32_t* argmax,
+                               const float* tau, const float* p_psi, float tau_psi,
+                               uint8_t* masked, int32_t* tokens, uint8_t* unmask,
+                               int32_t* n_commit, uint8_t* resolved, eb_stream_t stream) {
+  eb_status st = check_unmask(r, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved);
+  if (st != EB_OK) return st;
+  if (r->total_block > 0 && !p_psi) return fail(EB_ERR_INVALID, "NULL p_psi");
+  return hip_status(eb::unmask_select_lps(r->batch, r->cu_block, conf, argmax, tau, p_psi,
+                                          tau_psi, masked, tokens, unmask, n_commit, resolved,
+                                          stream),
+                    "eb_unmask_select_lps launch");
+}
+
+eb_status eb_unmask_select_topm(const eb_ragged* r, const float* conf, const int32_t* argmax,
+                                const float* tau, int32_t m, uint8_t* masked, int32_t* tokens,
+                                uint8_t* unmask, int32_t* n_commit, uint8_t* resolved,
+                                eb_stream_t stream) {
+  eb_status st = check_unmask(r, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved);
+  if (st != EB_OK) return st;
+  if (m < 0) return fail(EB_ERR_INVALID, "m must be >= 0 (got %d)", m);
+  return hip_status(eb::unmask_select_topm(r->batch, r->cu_block, conf, argmax, tau, m, masked,
+                                           tokens, unmask, n_commit, resolved, stream),
+                    "eb_unmask_select_topm launch");
 }
 
 eb_status eb_unmask_select(const eb_ragged* r, const float* conf, const int32_t* argmax,
@@ -225,13 +293,13 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
 
   if (tr) e = mark(tr->lmhead_begin);
   if (e == hipSuccess && T > 0)
-    e = eb::lmhead_partials(bf16, T, d->hidden, d->vocab, d->h, d->w, lm_ws, stream);
+    e = eb::lmhead_partials(bf16, T, d->hidden, d->vocab, d->h, d->w, lm_ws, false, stream);
   if (e == hipSuccess && tr) e = mark(tr->lmhead_end);
   if (e != hipSuccess) return hip_status(e, "step LM-head launch");
   if (tr) e = mark(tr->select_begin);
   if (e == hipSuccess && T > 0)
-    e = eb::lmhead_combine(T, eb::lmhead_num_slices(bf16, T, d->vocab), lm_ws, d->conf,
-                           d->entropy_nats, d->argmax, d->max_logit, stream);
+    e = eb::lmhead_combine(bf16, T, d->vocab, lm_ws, d->conf, d->entropy_nats, d->argmax,
+                           d->max_logit, nullptr, stream);
   if (e == hipSuccess)
     e = eb::unmask_select(r->batch, r->max_block, r->cu_block, d->conf, d->argmax, d->tau,
                           d->masked, d->tokens, d->unmask, d->n_commit, d->resolved, stream);

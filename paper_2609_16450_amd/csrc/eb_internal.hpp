@@ -11,12 +11,15 @@ namespace eb {
 // ---- LM head + confidence -------------------------------------------------------------
 // Number of vocabulary slices whose per-row partials are written to the workspace.
 int lmhead_num_slices(bool bf16, int n_rows, int vocab);
-size_t lmhead_ws_bytes(bool bf16, int n_rows, int vocab);
-// Partials [n_rows, n_slices] go to ws; the combine writes the per-row outputs.
+// With top2 the workspace also holds each partial's second-largest logit.
+size_t lmhead_ws_bytes(bool bf16, int n_rows, int vocab, bool top2);
+// Partials [n_rows, n_slices] go to ws; the combine writes the per-row outputs (top2_gap only
+// when the partials were formed with top2).
 hipError_t lmhead_partials(bool bf16, int n_rows, int hidden, int vocab, const void* h,
-                           const void* w, void* ws, hipStream_t s);
-hipError_t lmhead_combine(int n_rows, int n_slices, const void* ws, float* conf,
-                          float* entropy, int32_t* argmax, float* max_logit, hipStream_t s);
+                           const void* w, void* ws, bool top2, hipStream_t s);
+hipError_t lmhead_combine(bool bf16, int n_rows, int vocab, const void* ws, float* conf,
+                          float* entropy, int32_t* argmax, float* max_logit, float* top2_gap,
+                          hipStream_t s);
 
 // ---- block attention ------------------------------------------------------------------
 struct AttnArgs {
@@ -39,5 +42,16 @@ hipError_t unmask_select(int batch, int max_block, const int32_t* cu_block, cons
                          const int32_t* argmax, const float* tau, uint8_t* masked,
                          int32_t* tokens, uint8_t* unmask, int32_t* n_commit, uint8_t* resolved,
                          hipStream_t s);
+hipError_t unmask_select_lps(int batch, const int32_t* cu_block, const float* conf,
+                             const int32_t* argmax, const float* tau, const float* p_psi,
+                             float tau_psi, uint8_t* masked, int32_t* tokens, uint8_t* unmask,
+                             int32_t* n_commit, uint8_t* resolved, hipStream_t s);
+hipError_t unmask_select_topm(int batch, const int32_t* cu_block, const float* conf,
+                              const int32_t* argmax, const float* tau, int m, uint8_t* masked,
+                              int32_t* tokens, uint8_t* unmask, int32_t* n_commit,
+                              uint8_t* resolved, hipStream_t s);
+hipError_t lps_features(int batch, const int32_t* cu_block, int vocab, const float* conf,
+                        const float* entropy, const float* gap, const uint8_t* masked,
+                        float* feat, float* pos, float* mask_ratio, hipStream_t s);
 
 }  // namespace eb

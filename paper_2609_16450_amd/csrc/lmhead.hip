@@ -30,179 +30,33 @@ constexpr int kStreamThreads = kStreamWaves * 64;
 #endif
 constexpr int kStreamGroups = EB_STREAM_GROUPS;  // workgroups (256: one per compute unit)
 
-template <int TM, int NT, int kDepth>
-__global__ __launch_bounds__(kStreamThreads) void lmhead_stream_kernel(
-    const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
-    int vocab, int rows_per_wg, Partial* __restrict__ part, int n_slices) {
-  constexpr int KC = 512 / NT;         // h columns per LDS chunk
-  constexpr int kPitch = KC + 8;       // LDS row pitch (bf16)
-  constexpr int kSpc = KC / 16;        // k-steps per chunk
-  constexpr int kHRows = NT * 32;
-  constexpr int kHChunks16 = kHRows * KC / 8;  // 16-byte pieces per h chunk
-  constexpr int kHPer = kHChunks16 / kStreamThreads;
-  static_assert(kHChunks16 % kStreamThreads == 0, "h chunk splits evenly");
-  static_assert(kSpc % kDepth == 0, "chunk boundary falls on a group boundary");
-  __shared__ __attribute__((aligned(16))) uint16_t hs[2][kHRows * kPitch];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int half = lane >> 5, l32 = lane & 31;
-  const int wg = blockIdx.x;
-  const int vb = wg * rows_per_wg;
-  const int ve = min(vocab, vb + rows_per_wg);
-  const int rw = (rows_per_wg + kStreamWaves - 1) / kStreamWaves;
-  const int wb = vb + wave * rw;
-  const int we = min(ve, wb + rw);
-
-  // Every global load below is unconditional with a clamped address (a conditional load would
-  // make the compiler wait for it on the spot and serialise the stream).  Lanes past the end
-  // of the wave's rows re-read its last row (a cache hit); their sums are discarded.
-  const int wlast = max(min(we, vocab) - 1, 0);
-  const uint16_t* wp[TM];
-#pragma unroll
-  for (int tm = 0; tm < TM; ++tm) {
-    const int row = min(wb + tm * 32 + l32, wlast);
-    wp[tm] = w + static_cast<size_t>(row) * hidden + 8 * half;
-  }
-  const int nsteps = hidden / 16;
-  // The k-loop runs over whole groups of kDepth steps; steps past the end re-read the last
-  // real step of W (addresses stay in bounds) and meet h columns that are zero in LDS.
-  const int nsteps_p = (nsteps + kDepth - 1) / kDepth * kDepth;
-  const int nchunks = (hidden + KC - 1) / KC;
-
-  u32x4 buf[kDepth][TM];
-  auto issue = [&](int j, int step) {
-    const int st = min(step, nsteps - 1);
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm) buf[j][tm] = *reinterpret_cast<const u32x4*>(wp[tm] + 16 * st);
-  };
-
-  // h pieces: rows past n_rows re-read row n_rows - 1 (their columns of the product are
-  // discarded); columns past hidden are zeroed when stored to LDS.
-  u32x4 hreg[kHPer];
-  auto load_h = [&](int c) {
-#pragma unroll
-    for (int i = 0; i < kHPer; ++i) {
-      const int idx = tid + i * kStreamThreads;
-      const int row = min(idx / (KC / 8), n_rows - 1);
-      const int col = min(c * KC + (idx % (KC / 8)) * 8, hidden - 8);
-      hreg[i] = *reinterpret_cast<const u32x4*>(h + static_cast<size_t>(row) * hidden + col);
-    }
-  };
-  auto store_h = [&](int b, int c) {
-#pragma unroll
-    for (int i = 0; i < kHPer; ++i) {
-      const int idx = tid + i * kStreamThreads;
-      const int row = idx / (KC / 8), col = (idx % (KC / 8)) * 8;
-      const bool ok = c * KC + col < hidden;
-      *reinterpret_cast<u32x4*>(&hs[b][row * kPitch + col]) = ok ? hreg[i] : u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-
-  f32x16 acc[TM][NT];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < NT; ++b) acc[a][b] = f32x16{};
-
-#pragma unroll
-  for (int j = 0; j < kDepth; ++j) issue(j, j);
-  load_h(0);
-  store_h(0, 0);
-  __syncthreads();
-  if (nchunks > 1) load_h(1);
-
-  auto consume = [&](int g, int j) {
-    const uint16_t* hb = hs[(g / kSpc) & 1] + (g % kSpc) * 16 + 8 * half + 16 * j;
-    bf16x8 b[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      b[nt] = *reinterpret_cast<const bf16x8*>(hb + (nt * 32 + l32) * kPitch);
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      const bf16x8 a = __builtin_bit_cast(bf16x8, buf[j][tm]);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[tm][nt] = mfma32(a, b[nt], acc[tm][nt]);
-    }
-  };
-  auto chunk_boundary = [&](int g) {
-    if (g > 0 && g % kSpc == 0) {
-      // Entering chunk c: its h pieces were fetched during chunk c-1; the buffer they go to
-      // was last read during chunk c-2, before the barrier that opened chunk c-1.
-      const int c = g / kSpc;
-      store_h(c & 1, c);
-      __syncthreads();
-      if (c + 1 < nchunks) load_h(c + 1);
-    }
-  };
-
-  for (int g = 0; g < nsteps_p - kDepth; g += kDepth) {
-    chunk_boundary(g);
-#pragma unroll
-    for (int j = 0; j < kDepth; ++j) {
-      consume(g, j);
-      issue(j, g + kDepth + j);
-    }
-  }
-  chunk_boundary(nsteps_p - kDepth);
-#pragma unroll
-  for (int j = 0; j < kDepth; ++j) consume(nsteps_p - kDepth, j);
-
-  // Epilogue: per-lane partial over this wave's rows for its position, then across waves.
-  __syncthreads();  // all h reads done; reuse LDS for the cross-wave reduction
-  Partial* red = reinterpret_cast<Partial*>(&hs[0][0]);  // [kStreamWaves][kHRows]
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    float m = kNegBig;
-    int32_t idx = kNoIndex;
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = wb + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        const float z = acc[tm][nt][r];
-        if (v < we && z > m) {
-          m = z;
-          idx = v;
-        }
-      }
-    float s = 0.f, t = 0.f;
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = wb + tm * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (v < we) {
-          const float y = (acc[tm][nt][r] - m) * kLog2e;
-          const float e = fast_exp2(y);
-          s += e;
-          t = fmaf(e, y, t);
-        }
-      }
-    Partial p{m, s, t, idx};
-    p = partial_xor_merge(p, 32, lane);
-    if (lane < 32) red[wave * kHRows + nt * 32 + l32] = p;
-  }
-  __syncthreads();
-  if (tid < kHRows && tid < n_rows) {
-    Partial p = red[tid];
-#pragma unroll
-    for (int k = 1; k < kStreamWaves; ++k) p = partial_merge(p, red[k * kHRows + tid]);
-    part[static_cast<size_t>(tid) * n_slices + wg] = p;
-  }
-}
-
-// Same streaming scheme on 16x16x32 MFMA tiles.  A lane of the A operand holds 8 consecutive
+// The streaming kernel uses 16x16x32 MFMA tiles.  A lane of the A operand holds 8 consecutive
 // k-values of row l % 16 and the four lanes of a row cover 64 contiguous bytes, so each load
-// instruction reads 16 rows x 64 B of W (twice the run length of the 32x32 layout).
-// Lane l of the f32x4 accumulator holds C[4 (l / 16) + r][l % 16].
+// instruction reads 16 rows x 64 B of W (a 32x32x16 layout reads half that run per row and
+// measured 4.65 TB/s at best against 5.4).  Lane l of the f32x4 accumulator holds
+// C[4 (l / 16) + r][l % 16].
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-template <int TM, int NT, int kDepth>  // TM 16-row tiles per wave, NT 16-position tiles
+// Second-largest logit (with multiplicity) of the union of two sets whose largest values are
+// m_a, m_b and second-largest m2_a, m2_b.  Exact and order-free, so every merge order gives
+// the same bits.  kNegBig stands for "none".
+__device__ __forceinline__ float top2_merge(float m_a, float m2_a, float m_b, float m2_b) {
+  return fmaxf(fminf(m_a, m_b), fmaxf(m2_a, m2_b));
+}
+
+// top2_merge of a lane's (m, m2) with the lane `mask` away.
+__device__ __forceinline__ float top2_shfl_merge(float m, float m2, int mask) {
+  return top2_merge(m, m2, __shfl_xor(m, mask), __shfl_xor(m2, mask));
+}
+
+// kTop2: also track the second-largest logit of each (row, slice) into part2.
+template <int TM, int NT, int kDepth, bool kTop2>  // TM 16-row tiles per wave, NT 16-position tiles
 __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
-    int vocab, int rows_per_wg, Partial* __restrict__ part, int n_slices) {
+    int vocab, int rows_per_wg, Partial* __restrict__ part, float* __restrict__ part2,
+    int n_slices) {
   constexpr int KC = 1024 / NT;        // h columns per LDS chunk
   constexpr int kPitch = KC + 8;       // LDS row pitch (bf16)
   constexpr int kSpc = KC / 32;        // k-steps per chunk
@@ -309,9 +163,11 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
 
   __syncthreads();
   Partial* red = reinterpret_cast<Partial*>(&hs[0][0]);  // [kStreamWaves][kHRows]
+  float* red2 = reinterpret_cast<float*>(red + kStreamWaves * kHRows);
+  static_assert(kStreamWaves * kHRows * (sizeof(Partial) + 4) <= sizeof(hs), "reduction fits");
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    float m = kNegBig;
+    float m = kNegBig, m2 = kNegBig;
     int32_t idx = kNoIndex;
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
@@ -319,6 +175,7 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
       for (int r = 0; r < 4; ++r) {
         const int v = wb + tm * 16 + 4 * grp + r;
         const float z = acc[tm][nt][r];
+        if (kTop2 && v < we) m2 = fmaxf(m2, fminf(m, z));
         if (v < we && z > m) {
           m = z;
           idx = v;
@@ -338,31 +195,37 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
         }
       }
     Partial p{m, s, t, idx};
+    if (kTop2) m2 = top2_shfl_merge(p.m, m2, 16);
     p = partial_xor_merge(p, 16, lane);
+    if (kTop2) m2 = top2_shfl_merge(p.m, m2, 32);
     p = partial_xor_merge(p, 32, lane);
-    if (lane < 16) red[wave * kHRows + nt * 16 + l16] = p;
+    if (lane < 16) {
+      red[wave * kHRows + nt * 16 + l16] = p;
+      if (kTop2) red2[wave * kHRows + nt * 16 + l16] = m2;
+    }
   }
   __syncthreads();
   if (tid < kHRows && tid < n_rows) {
     Partial p = red[tid];
+    float m2 = kTop2 ? red2[tid] : kNegBig;
 #pragma unroll
-    for (int k = 1; k < kStreamWaves; ++k) p = partial_merge(p, red[k * kHRows + tid]);
+    for (int k = 1; k < kStreamWaves; ++k) {
+      const Partial q = red[k * kHRows + tid];
+      if (kTop2) m2 = top2_merge(p.m, m2, q.m, red2[k * kHRows + tid]);
+      p = partial_merge(p, q);
+    }
     part[static_cast<size_t>(tid) * n_slices + wg] = p;
+    if (kTop2) part2[static_cast<size_t>(tid) * n_slices + wg] = m2;
   }
 }
 
-// Streaming variant: MFMA tile shape (16 = 16x16x32, 32 = 32x32x16) and k-steps of W loads
-// in flight per wave.  Defaults come from measurement on MI355X (see the build notes); the
-// macros exist so that other settings can be built and timed.
-#ifndef EB_STREAM_SHAPE
-#define EB_STREAM_SHAPE 16
-#endif
+// k-steps of W loads in flight per wave (measured on MI355X; the macro exists so that other
+// settings can be built and timed).
 #ifndef EB_STREAM_DEPTH
 #define EB_STREAM_DEPTH 2
 #endif
-constexpr int kStreamShape = EB_STREAM_SHAPE;
+constexpr int kStreamShape = 16;  // rows (and positions) per MFMA tile
 constexpr int kStreamDepth = EB_STREAM_DEPTH;
-static_assert(kStreamShape == 16 || kStreamShape == 32, "EB_STREAM_SHAPE is 16 or 32");
 
 struct StreamPlan {
   int groups, rows_per_wg, tm;  // tm: MFMA row tiles per wave
@@ -376,71 +239,58 @@ StreamPlan stream_plan(int vocab) {
 }
 
 constexpr int kStreamMaxRows = 64;  // n_rows handled by the streaming kernel
-constexpr int kStreamMaxTm = kStreamShape == 16 ? 8 : 4;
+constexpr int kStreamMaxTm = 8;
 
 bool use_stream(int n_rows, int vocab) {
   if (n_rows > kStreamMaxRows) return false;
   const int tm = stream_plan(vocab).tm;
-  if (n_rows > 2 * kStreamShape) return tm <= (kStreamShape == 16 ? 6 : 3);  // register budget
+  if (n_rows > 2 * kStreamShape) return tm <= 6;  // register budget with four position tiles
   return tm <= kStreamMaxTm;
 }
 
-template <int TM, int NT>
+template <int TM, int NT, bool kTop2>
 hipError_t launch_stream_tm(int n_rows, int hidden, int vocab, const StreamPlan& pl,
-                            const void* h, const void* w, Partial* part, hipStream_t s) {
-  if constexpr (kStreamShape == 16) {
-    constexpr int D = (kStreamDepth * TM > 16) ? (16 / TM > 0 ? 16 / TM : 1) : kStreamDepth;
-    constexpr int Dp = D >= 4 ? 4 : (D >= 2 ? 2 : 1);  // divides the per-chunk step count
-    hipLaunchKernelGGL((lmhead_stream16_kernel<TM, NT, Dp>), dim3(pl.groups),
-                       dim3(kStreamThreads), 0, s, static_cast<const uint16_t*>(h),
-                       static_cast<const uint16_t*>(w), n_rows, hidden, vocab, pl.rows_per_wg,
-                       part, pl.groups);
-  } else {
-    constexpr int D = (kStreamDepth * TM > 16) ? (16 / TM) : kStreamDepth;
-    constexpr int Dp = D >= 8 ? 8 : (D >= 4 ? 4 : 2);
-    hipLaunchKernelGGL((lmhead_stream_kernel<TM, NT, Dp>), dim3(pl.groups), dim3(kStreamThreads),
-                       0, s, static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w),
-                       n_rows, hidden, vocab, pl.rows_per_wg, part, pl.groups);
-  }
+                            const void* h, const void* w, Partial* part, float* part2,
+                            hipStream_t s) {
+  constexpr int D = (kStreamDepth * TM > 16) ? (16 / TM > 0 ? 16 / TM : 1) : kStreamDepth;
+  constexpr int Dp = D >= 4 ? 4 : (D >= 2 ? 2 : 1);  // divides the per-chunk step count
+  hipLaunchKernelGGL((lmhead_stream16_kernel<TM, NT, Dp, kTop2>), dim3(pl.groups),
+                     dim3(kStreamThreads), 0, s, static_cast<const uint16_t*>(h),
+                     static_cast<const uint16_t*>(w), n_rows, hidden, vocab, pl.rows_per_wg, part,
+                     part2, pl.groups);
   return hipGetLastError();
 }
 
-// NT: position tiles (of 16 or 32 positions) covering n_rows.
-template <int NT>
+// NT: 16-position tiles covering n_rows.
+template <int NT, bool kTop2>
 hipError_t launch_stream(int n_rows, int hidden, int vocab, const void* h, const void* w,
-                         Partial* part, hipStream_t s) {
+                         Partial* part, float* part2, hipStream_t s) {
   const StreamPlan pl = stream_plan(vocab);
   switch (pl.tm) {
-    case 1: return launch_stream_tm<1, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
-    case 2: return launch_stream_tm<2, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
-    case 3: return launch_stream_tm<3, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
-    case 4:
-      if constexpr (kStreamShape == 16 || NT == 1)
-        return launch_stream_tm<4, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
-      return hipErrorInvalidValue;
-    case 5:
-    case 6:
+    case 1: return launch_stream_tm<1, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+    case 2: return launch_stream_tm<2, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+    case 3: return launch_stream_tm<3, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+    case 4: return launch_stream_tm<4, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+    case 5: return launch_stream_tm<5, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+    case 6: return launch_stream_tm<6, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
     case 7:
+      if constexpr (NT < 4)
+        return launch_stream_tm<7, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+      return hipErrorInvalidValue;
     case 8:
-      if constexpr (kStreamShape == 16) {
-        if (pl.tm == 5) return launch_stream_tm<5, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
-        if (pl.tm == 6) return launch_stream_tm<6, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
-        if (pl.tm == 7) return launch_stream_tm<7, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
-        return launch_stream_tm<8, NT>(n_rows, hidden, vocab, pl, h, w, part, s);
-      }
+      if constexpr (NT < 4)
+        return launch_stream_tm<8, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
       return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;  // excluded by use_stream
   }
 }
 
+template <bool kTop2>
 hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, const void* w,
-                              Partial* part, hipStream_t s) {
-  constexpr int kTile = kStreamShape;
-  if (n_rows <= kTile) return launch_stream<1>(n_rows, hidden, vocab, h, w, part, s);
-  if (n_rows <= 2 * kTile) return launch_stream<2>(n_rows, hidden, vocab, h, w, part, s);
-  if constexpr (kStreamShape == 16) {
-    if (n_rows <= 4 * kTile) return launch_stream<4>(n_rows, hidden, vocab, h, w, part, s);
-  }
+                              Partial* part, float* part2, hipStream_t s) {
+  if (n_rows <= 16) return launch_stream<1, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s);
+  if (n_rows <= 32) return launch_stream<2, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s);
+  if (n_rows <= 64) return launch_stream<4, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s);
   return hipErrorInvalidValue;  // excluded by use_stream
 }
 
@@ -520,18 +370,28 @@ __device__ __forceinline__ void wait_stage(int later) {
 // r % 4) carry the max, the sums and the first argmax, so the reduction is not bound by the
 // latency of one long dependency chain; each chain walks its rows in decreasing order, so its
 // last z == max hit is its lowest row, and the chains are combined at the end.
-template <int TM, int TN>
+// With kTop2 the max pass also tracks each chain's second-largest logit; m2 returns the
+// lane's second-largest (kNegBig if none).
+template <int TM, int TN, bool kTop2 = false>
 __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], int tn, int vbase,
-                                                  int vocab, bool full) {
+                                                  int vocab, bool full, float* m2 = nullptr) {
   float mc[4] = {kNegBig, kNegBig, kNegBig, kNegBig};
+  float mc2[4] = {kNegBig, kNegBig, kNegBig, kNegBig};
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int v = vbase + tm * 32 + 8 * (r >> 2) + (r & 3);
-      if (full || v < vocab) mc[r & 3] = fmaxf(mc[r & 3], acc[tm][tn][r]);
+      if (full || v < vocab) {
+        const float z = acc[tm][tn][r];
+        if (kTop2) mc2[r & 3] = fmaxf(mc2[r & 3], fminf(mc[r & 3], z));
+        mc[r & 3] = fmaxf(mc[r & 3], z);
+      }
     }
   const float m = fmaxf(fmaxf(mc[0], mc[1]), fmaxf(mc[2], mc[3]));
+  if (kTop2)
+    *m2 = top2_merge(fmaxf(mc[0], mc[1]), top2_merge(mc[0], mc2[0], mc[1], mc2[1]),
+                     fmaxf(mc[2], mc[3]), top2_merge(mc[2], mc2[2], mc[3], mc2[3]));
   float sc[4] = {0.f, 0.f, 0.f, 0.f}, tc[4] = {0.f, 0.f, 0.f, 0.f};
   int32_t ic[4] = {kNoIndex, kNoIndex, kNoIndex, kNoIndex};
 #pragma unroll
@@ -553,10 +413,11 @@ __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], i
                  min(min(ic[0], ic[1]), min(ic[2], ic[3]))};
 }
 
-template <int WN, int BN, int RING, int MINB>
+template <int WN, int BN, int RING, int MINB, bool kTop2>
 __global__ __launch_bounds__(128 * WN, MINB) void lmhead_tile_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
-    int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part) {
+    int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part,
+    float* __restrict__ part2) {
   constexpr int BM = kTileBM, BK = kTileBK;
   constexpr int WM = 2, kWaves = WM * WN;
   constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
@@ -650,21 +511,36 @@ __global__ __launch_bounds__(128 * WN, MINB) void lmhead_tile_kernel(
   // Epilogue: per-lane partial for its position column, merged with the other half of the
   // wave, then with the other vocabulary wave through LDS.
   Partial* red = reinterpret_cast<Partial*>(smem);  // [WM][BN]
+  float* red2 = reinterpret_cast<float*>(red + WM * BN);
+  static_assert(WM * BN * (sizeof(Partial) + 4) <= sizeof(smem), "reduction fits in LDS");
   const bool full = v0 + BM <= vocab;
   const int vbase = v0 + wm * kWaveM + 4 * half;
 #pragma unroll
   for (int tn = 0; tn < TN; ++tn) {
-    Partial p = column_partial<TM, TN>(acc, tn, vbase, vocab, full);
+    float m2 = kNegBig;
+    Partial p = column_partial<TM, TN, kTop2>(acc, tn, vbase, vocab, full, &m2);
+    if (kTop2) m2 = top2_shfl_merge(p.m, m2, 32);
     p = partial_xor_merge(p, 32, lane);
-    if (lane < 32) red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
+    if (lane < 32) {
+      red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
+      if (kTop2) red2[wm * BN + wn * kWaveN + tn * 32 + l32] = m2;
+    }
   }
   __syncthreads();
   for (int c = tid; c < BN; c += kWaves * 64) {
     Partial p = red[c];
+    float m2 = kTop2 ? red2[c] : kNegBig;
 #pragma unroll
-    for (int q = 1; q < WM; ++q) p = partial_merge(p, red[q * BN + c]);
+    for (int q = 1; q < WM; ++q) {
+      const Partial o = red[q * BN + c];
+      if (kTop2) m2 = top2_merge(p.m, m2, o.m, red2[q * BN + c]);
+      p = partial_merge(p, o);
+    }
     const int row = r0 + c;
-    if (row < n_rows) part[static_cast<size_t>(row) * n_vtiles + vt] = p;
+    if (row < n_rows) {
+      part[static_cast<size_t>(row) * n_vtiles + vt] = p;
+      if (kTop2) part2[static_cast<size_t>(row) * n_vtiles + vt] = m2;
+    }
   }
 }
 
@@ -684,10 +560,11 @@ __device__ __forceinline__ void wait_vm_lds_and_barrier() {
 // double-buffered in registers: the reads of one half are issued before the MFMAs of the
 // other, so LDS latency hides under 16 MFMAs.  The DMA ring keeps RING stages occupied: right
 // after the barrier that ends the reads of stage kt, stage kt + RING is issued into its slot.
-template <int RING>
+template <int RING, bool kTop2>
 __global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
-    int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part) {
+    int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part,
+    float* __restrict__ part2) {
   constexpr int BM = kTileBM, BN = 256, BK = kTileBK;
   constexpr int WM = 2, WN = 2, kWaves = WM * WN;
   constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
@@ -808,21 +685,36 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
   wait_vm_lds_and_barrier<0>();  // no DMA in flight; every wave is done reading the ring
 
   Partial* red = reinterpret_cast<Partial*>(smem);  // [WM][BN]
+  float* red2 = reinterpret_cast<float*>(red + WM * BN);
+  static_assert(WM * BN * (sizeof(Partial) + 4) <= sizeof(smem), "reduction fits in LDS");
   const bool full = v0 + BM <= vocab;
   const int vbase = v0 + wm * kWaveM + 4 * half;
 #pragma unroll
   for (int tn = 0; tn < TN; ++tn) {
-    Partial p = column_partial<TM, TN>(acc, tn, vbase, vocab, full);
+    float m2 = kNegBig;
+    Partial p = column_partial<TM, TN, kTop2>(acc, tn, vbase, vocab, full, &m2);
+    if (kTop2) m2 = top2_shfl_merge(p.m, m2, 32);
     p = partial_xor_merge(p, 32, lane);
-    if (lane < 32) red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
+    if (lane < 32) {
+      red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
+      if (kTop2) red2[wm * BN + wn * kWaveN + tn * 32 + l32] = m2;
+    }
   }
   __syncthreads();
   for (int c = tid; c < BN; c += kWaves * 64) {
     Partial p = red[c];
+    float m2 = kTop2 ? red2[c] : kNegBig;
 #pragma unroll
-    for (int q = 1; q < WM; ++q) p = partial_merge(p, red[q * BN + c]);
+    for (int q = 1; q < WM; ++q) {
+      const Partial o = red[q * BN + c];
+      if (kTop2) m2 = top2_merge(p.m, m2, o.m, red2[q * BN + c]);
+      p = partial_merge(p, o);
+    }
     const int row = r0 + c;
-    if (row < n_rows) part[static_cast<size_t>(row) * n_vtiles + vt] = p;
+    if (row < n_rows) {
+      part[static_cast<size_t>(row) * n_vtiles + vt] = p;
+      if (kTop2) part2[static_cast<size_t>(row) * n_vtiles + vt] = m2;
+    }
   }
 }
 
@@ -841,20 +733,23 @@ constexpr int kTileBN = EB_TILE_VARIANT == 1 ? 128 : 256;
 static_assert(EB_TILE_VARIANT == 1 || EB_TILE_VARIANT == 2 || EB_TILE_VARIANT == 5,
               "tile variant");
 
+template <bool kTop2>
 hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const void* w,
-                       Partial* part, hipStream_t s) {
+                       Partial* part, float* part2, hipStream_t s) {
   const TileMap m = tile_map(n_rows, vocab, kTileBN);
   const uint16_t* hp = static_cast<const uint16_t*>(h);
   const uint16_t* wp = static_cast<const uint16_t*>(w);
   if constexpr (EB_TILE_VARIANT == 1) {
-    hipLaunchKernelGGL((lmhead_tile_kernel<2, 128, 3, 2>), dim3(m.grid), dim3(256), 0, s, hp, wp,
-                       n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
+    hipLaunchKernelGGL((lmhead_tile_kernel<2, 128, 3, 2, kTop2>), dim3(m.grid), dim3(256), 0, s,
+                       hp, wp, n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part,
+                       part2);
   } else if constexpr (EB_TILE_VARIANT == 5) {
-    hipLaunchKernelGGL((lmhead_tile4_kernel<4>), dim3(m.grid), dim3(256), 0, s, hp, wp, n_rows,
-                       hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
+    hipLaunchKernelGGL((lmhead_tile4_kernel<4, kTop2>), dim3(m.grid), dim3(256), 0, s, hp, wp,
+                       n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part, part2);
   } else {
-    hipLaunchKernelGGL((lmhead_tile_kernel<4, 256, 4, 1>), dim3(m.grid), dim3(512), 0, s, hp, wp,
-                       n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part);
+    hipLaunchKernelGGL((lmhead_tile_kernel<4, 256, 4, 1, kTop2>), dim3(m.grid), dim3(512), 0, s,
+                       hp, wp, n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part,
+                       part2);
   }
   return hipGetLastError();
 }
@@ -864,18 +759,22 @@ hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const v
 // ---------------------------------------------------------------------------------------
 constexpr int kF32SliceRows = 256;
 
+template <bool kTop2>
 __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict__ h,
                                                          const float* __restrict__ w,
                                                          int n_rows, int hidden, int vocab,
                                                          int n_slices,
-                                                         Partial* __restrict__ part) {
+                                                         Partial* __restrict__ part,
+                                                         float* __restrict__ part2) {
   __shared__ Partial red[4];
+  __shared__ float red2[4];
   const int slice = blockIdx.x;
   const int row = blockIdx.y;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int v = slice * kF32SliceRows + threadIdx.x;
   Partial p = partial_empty();
+  float m2 = kNegBig;
   if (v < vocab) {
     const float* wr = w + static_cast<size_t>(v) * hidden;
     const float* hr = h + static_cast<size_t>(row) * hidden;
@@ -883,34 +782,67 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
     for (int k = 0; k < hidden; ++k) z = fmaf(wr[k], hr[k], z);
     p = Partial{z, 1.f, 0.f, v};
   }
-  for (int mask = 32; mask >= 1; mask >>= 1) p = partial_xor_merge(p, mask, lane);
-  if (lane == 0) red[wave] = p;
+  for (int mask = 32; mask >= 1; mask >>= 1) {
+    if (kTop2) m2 = top2_shfl_merge(p.m, m2, mask);
+    p = partial_xor_merge(p, mask, lane);
+  }
+  if (lane == 0) {
+    red[wave] = p;
+    red2[wave] = m2;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     Partial q = red[0];
-    for (int k = 1; k < 4; ++k) q = partial_merge(q, red[k]);
+    float q2 = red2[0];
+    for (int k = 1; k < 4; ++k) {
+      if (kTop2) q2 = top2_merge(q.m, q2, red[k].m, red2[k]);
+      q = partial_merge(q, red[k]);
+    }
     part[static_cast<size_t>(row) * n_slices + slice] = q;
+    if (kTop2) part2[static_cast<size_t>(row) * n_slices + slice] = q2;
   }
 }
 
 // ---------------------------------------------------------------------------------------
 // combine: one wavefront per row, fixed merge order (lane-strided, then butterfly)
 // ---------------------------------------------------------------------------------------
+template <bool kTop2>
 __global__ __launch_bounds__(256) void lmhead_combine_kernel(const Partial* __restrict__ part,
+                                                             const float* __restrict__ part2,
                                                              int n_rows, int n_slices,
                                                              float* __restrict__ conf,
                                                              float* __restrict__ entropy,
                                                              int32_t* __restrict__ argmax,
-                                                             float* __restrict__ max_logit) {
+                                                             float* __restrict__ max_logit,
+                                                             float* __restrict__ top2_gap) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n_rows) return;  // uniform per wavefront
-  const Partial p = wave_merge(part + static_cast<size_t>(row) * n_slices, n_slices, lane);
+  const Partial* pr = part + static_cast<size_t>(row) * n_slices;
+  const Partial p = wave_merge(pr, n_slices, lane);
+  float m2 = kNegBig;
+  if (kTop2) {
+    // (max, second max) over the slices: lane-strided, then a butterfly; exact in any order
+    float m = kNegBig;
+    const float* p2 = part2 + static_cast<size_t>(row) * n_slices;
+    for (int j = lane; j < n_slices; j += 64) {
+      const float mj = pr[j].m;
+      m2 = top2_merge(m, m2, mj, p2[j]);
+      m = fmaxf(m, mj);
+    }
+    for (int mask = 32; mask >= 1; mask >>= 1) {
+      m2 = top2_shfl_merge(m, m2, mask);
+      m = fmaxf(m, __shfl_xor(m, mask));
+    }
+  }
   if (lane == 0) {
-    conf[row] = 1.0f / p.s;
+    const float inv = 1.0f / p.s;
+    conf[row] = inv;
     entropy[row] = logf(p.s) - kLn2 * p.t / p.s;
     argmax[row] = p.idx;
     if (max_logit) max_logit[row] = p.m;
+    // p_(1) - p_(2) = (1 - e^(z2 - m)) / s; 0 when the maximum is shared (z2 = m)
+    if (kTop2) top2_gap[row] = (1.0f - fast_exp2((m2 - p.m) * kLog2e)) * inv;
   }
 }
 
@@ -922,31 +854,63 @@ int lmhead_num_slices(bool bf16, int n_rows, int vocab) {
   return (vocab + kF32SliceRows - 1) / kF32SliceRows;
 }
 
-size_t lmhead_ws_bytes(bool bf16, int n_rows, int vocab) {
-  return static_cast<size_t>(n_rows) * lmhead_num_slices(bf16, n_rows, vocab) * sizeof(Partial);
+// Workspace: partials [n_rows, n_slices] (16 B each), then with top2 the second-largest logits
+// [n_rows, n_slices] (4 B each) from the next 256-byte boundary.
+static size_t lmhead_part_bytes(bool bf16, int n_rows, int vocab) {
+  const size_t b = static_cast<size_t>(n_rows) * lmhead_num_slices(bf16, n_rows, vocab) *
+                   sizeof(Partial);
+  return (b + 255) / 256 * 256;
+}
+
+size_t lmhead_ws_bytes(bool bf16, int n_rows, int vocab, bool top2) {
+  size_t b = lmhead_part_bytes(bf16, n_rows, vocab);
+  if (top2) b += static_cast<size_t>(n_rows) * lmhead_num_slices(bf16, n_rows, vocab) * 4;
+  return b;
 }
 
 hipError_t lmhead_partials(bool bf16, int n_rows, int hidden, int vocab, const void* h,
-                           const void* w, void* ws, hipStream_t s) {
+                           const void* w, void* ws, bool top2, hipStream_t s) {
   if (n_rows == 0) return hipSuccess;
   Partial* part = static_cast<Partial*>(ws);
+  float* part2 = top2 ? reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                                 lmhead_part_bytes(bf16, n_rows, vocab))
+                      : nullptr;
   if (!bf16) {
     const int n_slices = lmhead_num_slices(false, n_rows, vocab);
     dim3 grid(n_slices, n_rows);
-    hipLaunchKernelGGL(lmhead_f32_kernel, grid, dim3(256), 0, s, static_cast<const float*>(h),
-                       static_cast<const float*>(w), n_rows, hidden, vocab, n_slices, part);
+    const float* hp = static_cast<const float*>(h);
+    const float* wp = static_cast<const float*>(w);
+    if (top2)
+      hipLaunchKernelGGL(lmhead_f32_kernel<true>, grid, dim3(256), 0, s, hp, wp, n_rows, hidden,
+                         vocab, n_slices, part, part2);
+    else
+      hipLaunchKernelGGL(lmhead_f32_kernel<false>, grid, dim3(256), 0, s, hp, wp, n_rows, hidden,
+                         vocab, n_slices, part, part2);
     return hipGetLastError();
   }
-  if (use_stream(n_rows, vocab)) return launch_stream_rows(n_rows, hidden, vocab, h, w, part, s);
-  return launch_tile(n_rows, hidden, vocab, h, w, part, s);
+  if (use_stream(n_rows, vocab))
+    return top2 ? launch_stream_rows<true>(n_rows, hidden, vocab, h, w, part, part2, s)
+                : launch_stream_rows<false>(n_rows, hidden, vocab, h, w, part, part2, s);
+  return top2 ? launch_tile<true>(n_rows, hidden, vocab, h, w, part, part2, s)
+              : launch_tile<false>(n_rows, hidden, vocab, h, w, part, part2, s);
 }
 
-hipError_t lmhead_combine(int n_rows, int n_slices, const void* ws, float* conf,
-                          float* entropy, int32_t* argmax, float* max_logit, hipStream_t s) {
+hipError_t lmhead_combine(bool bf16, int n_rows, int vocab, const void* ws, float* conf,
+                          float* entropy, int32_t* argmax, float* max_logit, float* top2_gap,
+                          hipStream_t s) {
   if (n_rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(lmhead_combine_kernel, dim3((n_rows + 3) / 4), dim3(256), 0, s,
-                     static_cast<const Partial*>(ws), n_rows, n_slices, conf, entropy, argmax,
-                     max_logit);
+  const int n_slices = lmhead_num_slices(bf16, n_rows, vocab);
+  const Partial* part = static_cast<const Partial*>(ws);
+  const dim3 grid((n_rows + 3) / 4);
+  if (top2_gap) {
+    const float* part2 = reinterpret_cast<const float*>(static_cast<const char*>(ws) +
+                                                        lmhead_part_bytes(bf16, n_rows, vocab));
+    hipLaunchKernelGGL(lmhead_combine_kernel<true>, grid, dim3(256), 0, s, part, part2, n_rows,
+                       n_slices, conf, entropy, argmax, max_logit, top2_gap);
+  } else {
+    hipLaunchKernelGGL(lmhead_combine_kernel<false>, grid, dim3(256), 0, s, part, nullptr,
+                       n_rows, n_slices, conf, entropy, argmax, max_logit, nullptr);
+  }
   return hipGetLastError();
 }
 

@@ -69,6 +69,31 @@ def test_invalid_arguments_are_rejected_before_launch():
     assert "workspace" in B.eb_last_error()
 
 
+def test_next_row_entry_points_reject_bad_arguments():
+    lib = B.load()
+    r = _ragged()
+    # the gap output is required
+    assert lib.eb_lmhead_features(B.EB_BF16, 4, 64, 1000, *([0x100] * 5), None, None, 0x100,
+                                  1 << 20, None) == B.EB_ERR_INVALID
+    assert "top2_gap" in B.eb_last_error()
+    # short workspace: the gap path needs more than the plain one
+    plain = lib.eb_lmhead_workspace(B.EB_BF16, 4, 64, 1000)
+    need = lib.eb_lmhead_features_workspace(B.EB_BF16, 4, 64, 1000)
+    assert need > plain
+    assert lib.eb_lmhead_features(B.EB_BF16, 4, 64, 1000, *([0x100] * 5), None, 0x100, 0x100,
+                                  need - 1, None) == B.EB_ERR_WORKSPACE
+    # vocab must allow ln(vocab) > 0; feat must be 16-byte aligned
+    assert lib.eb_lps_features(ctypes.byref(r), 1, *([0x100] * 6), None, None) == B.EB_ERR_INVALID
+    assert lib.eb_lps_features(ctypes.byref(r), 100, *([0x100] * 4), 0x104, 0x100, None,
+                               None) == B.EB_ERR_INVALID
+    # router score required; budget must not be negative
+    assert lib.eb_unmask_select_lps(ctypes.byref(r), 0x100, 0x100, 0x100, None, 0.9,
+                                    *([0x100] * 5), None) == B.EB_ERR_INVALID
+    assert lib.eb_unmask_select_topm(ctypes.byref(r), 0x100, 0x100, 0x100, -1, *([0x100] * 5),
+                                     None) == B.EB_ERR_INVALID
+    assert "m must be" in B.eb_last_error()
+
+
 def test_workspace_queries():
     lib = B.load()
     assert lib.eb_lmhead_workspace(B.EB_BF16, 0, 4096, 126464) == 0

@@ -1,0 +1,242 @@
+"""GPU parity of the next-row entry points against the fp64 oracle, through the C ABI:
+the LM head with the top-1/top-2 gap, the LPS features, the union accept rule and the top-m
+budget commit.
+
+Bars (written here, enforced below):
+  * argmax ids, unmask flags, committed tokens, mask flags, n_commit, resolved: bit-exact;
+  * kappa, raw entropy and the top-1/top-2 gap: within 1e-3 absolute (inputs carry the
+    away-from-tie margins of oracle/margins.py, so the two largest logits are >= 4e-3 apart);
+  * LPS features: kappa, H / ln V and the gap within 1e-3 of the oracle's fp64 values computed
+    from the same GPU statistics up to fp32 rounding (1e-6), the mask ratio and positions
+    within 1e-6.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_16450_amd import (Ragged, eb_lmhead_confidence, eb_lmhead_features,
+                                  eb_lps_features, eb_unmask_select_lps, eb_unmask_select_topm)
+from paper_2609_16450_amd.device_case import DeviceStep
+from tests._cases import as_f32, enforce_margins
+from workloads import CONFIGS, custom_config, make_step, router_scores
+
+pytestmark = pytest.mark.gpu
+
+STAT_ATOL = 1e-3
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _features_run(ds, T):
+    gap = torch.empty(T, dtype=torch.float32, device="cuda")
+    eb_lmhead_features(ds.h, ds.w, ds.conf, ds.entropy, ds.argmax, gap, ds.max_logit)
+    torch.cuda.synchronize()
+    return gap.cpu().numpy()
+
+
+LM_CASES = [
+    (1, 64, 1000, "bf16"),
+    (32, 320, 3000, "bf16"),
+    (64, 192, 4099, "bf16"),
+    (200, 512, 5000, "bf16"),
+    (600, 192, 9000, "bf16"),
+    (32, 256, 126464, "bf16"),
+    (48, 192, 152064, "bf16"),
+    (7, 100, 999, "f32"),
+]
+
+
+@pytest.mark.parametrize("n_rows,hidden,vocab,dt", LM_CASES)
+def test_lmhead_features_small(n_rows, hidden, vocab, dt):
+    say(f"lmhead features n_rows={n_rows} hidden={hidden} vocab={vocab} dtype={dt}")
+    cfg = custom_config(seed=311 + n_rows, block_len=("fixed", n_rows), hidden=hidden,
+                        vocab=vocab, dtype=dt, hq=1, hkv=1, head_dim=64, prefix_len=("fixed", 0))
+    case = enforce_margins(make_step(cfg))
+    ref = oracle.lmhead_confidence(as_f32(case.h, dt), as_f32(case.w, dt))
+    ds = DeviceStep(case)
+    gap = _features_run(ds, case.T)
+    np.testing.assert_array_equal(ds.argmax.cpu().numpy(), ref["argmax"])
+    np.testing.assert_allclose(ds.conf.cpu().numpy(), ref["conf"], rtol=0, atol=STAT_ATOL)
+    np.testing.assert_allclose(ds.entropy.cpu().numpy(), ref["entropy"], rtol=0, atol=STAT_ATOL)
+    np.testing.assert_allclose(gap, ref["top2_gap"], rtol=0, atol=STAT_ATOL)
+    # the statistics equal those of the plain entry point bit for bit
+    c0, e0, a0 = ds.conf.clone(), ds.entropy.clone(), ds.argmax.clone()
+    eb_lmhead_confidence(ds.h, ds.w, ds.conf, ds.entropy, ds.argmax, ds.max_logit)
+    torch.cuda.synchronize()
+    assert torch.equal(c0, ds.conf) and torch.equal(e0, ds.entropy) and torch.equal(a0, ds.argmax)
+
+
+@pytest.mark.parametrize("n_rows", [20, 300])
+def test_lmhead_gap_shared_maximum_is_zero(n_rows):
+    # duplicated W rows give bit-identical logits; where they hold the maximum the gap is 0
+    say(f"lmhead gap ties n_rows={n_rows}")
+    rng = np.random.default_rng(21)
+    d, V = 256, 3000
+    h = torch.from_numpy(rng.standard_normal((n_rows, d)).astype(np.float32)).to(torch.bfloat16)
+    w = torch.from_numpy((rng.standard_normal((V, d)) / 16).astype(np.float32)).to(torch.bfloat16)
+    w[2900] = (h.float().mean(0) * 4).to(torch.bfloat16)
+    w[130] = w[2900]
+    h, w = h.cuda(), w.cuda()
+    out = [torch.empty(n_rows, device="cuda") for _ in range(2)]
+    am = torch.empty(n_rows, dtype=torch.int32, device="cuda")
+    gap = torch.empty(n_rows, device="cuda")
+    eb_lmhead_features(h, w, out[0], out[1], am, gap)
+    torch.cuda.synchronize()
+    z = h.float().cpu().double().numpy() @ w.float().cpu().double().numpy().T
+    top = z.max(1)
+    shared = (z == top[:, None]).sum(1) > 1
+    assert shared.sum() > 0
+    np.testing.assert_array_equal(gap.cpu().numpy()[shared], 0.0)
+    np.testing.assert_array_equal(am.cpu().numpy()[shared], 130)
+
+
+def test_lps_features_random_ragged():
+    say("lps features")
+    rng = np.random.default_rng(22)
+    lens = [0, 1, 5, 32, 257, 1000, 3, 0, 64]
+    r = Ragged.from_lengths(lens, [0] * len(lens))
+    T = r.total_block
+    conf = rng.random(T).astype(np.float32)
+    ent = (rng.random(T) * 9).astype(np.float32)
+    gap = (rng.random(T) * conf).astype(np.float32)
+    masked = (rng.random(T) < 0.45).astype(np.uint8)
+    V = 152064
+    d = lambda x: torch.from_numpy(x).cuda()
+    feat = torch.full((T, 4), -7.0, device="cuda")
+    pos = torch.full((T,), -7.0, device="cuda")
+    rho = torch.full((len(lens),), -7.0, device="cuda")
+    eb_lps_features(r, V, d(conf), d(ent), d(gap), d(masked), feat, pos, rho)
+    torch.cuda.synchronize()
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    ref = oracle.lps_features(conf, ent, gap, masked, cu, V)
+    np.testing.assert_allclose(feat.cpu().numpy(), ref["feat"], rtol=1e-6, atol=1e-6)
+    np.testing.assert_allclose(pos.cpu().numpy(), ref["pos"], rtol=0, atol=1e-6)
+    np.testing.assert_allclose(rho.cpu().numpy(), ref["mask_ratio"], rtol=0, atol=1e-6)
+
+
+def _unmask_io(lens, conf, masked, argmax, tokens, tau):
+    d = lambda x, dt: torch.from_numpy(np.asarray(x, dtype=dt)).cuda()
+    B, T = len(lens), int(sum(lens))
+    return dict(conf=d(conf, np.float32), argmax=d(argmax, np.int32), tau=d(tau, np.float32),
+                masked=d(masked, np.uint8), tokens=d(tokens, np.int32),
+                unmask=torch.full((T,), 7, dtype=torch.uint8, device="cuda"),
+                n_commit=torch.full((B,), -5, dtype=torch.int32, device="cuda"),
+                resolved=torch.full((B,), 9, dtype=torch.uint8, device="cuda"))
+
+
+def _outputs(io):
+    torch.cuda.synchronize()
+    return {k: io[k].cpu().numpy() for k in ("unmask", "tokens", "masked", "n_commit", "resolved")}
+
+
+def _assert_same(got, ref):
+    for k in ("unmask", "tokens", "masked", "n_commit", "resolved"):
+        np.testing.assert_array_equal(got[k], ref[k], err_msg=k)
+
+
+def _random_blocks(rng, B, max_len, tie_grid=20):
+    lens = rng.integers(0, max_len, B).tolist()
+    T = sum(lens)
+    conf = (rng.integers(0, tie_grid, T) / tie_grid).astype(np.float32)
+    masked = (rng.random(T) < rng.random()).astype(np.uint8)
+    argmax = rng.integers(0, 152064, T).astype(np.int32)
+    tokens = np.where(masked == 1, -1, rng.integers(0, 152064, T)).astype(np.int32)
+    tau = rng.choice(np.array([0.7, 0.8, 0.9, 0.95], np.float32), B)
+    return lens, conf, masked, argmax, tokens, tau
+
+
+def test_unmask_lps_random_ragged():
+    say("unmask lps")
+    rng = np.random.default_rng(23)
+    for it in range(12):
+        lens, conf, masked, argmax, tokens, tau = _random_blocks(rng, int(rng.integers(1, 60)), 300)
+        T = sum(lens)
+        tau_psi = np.float32(0.95)
+        p_psi = rng.choice(np.array([0.1, 0.5, 0.95, 0.9500001, 0.99], np.float32), T)
+        cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        ref = oracle.unmask_select_lps(conf, argmax, masked, tokens, tau, cu, p_psi, tau_psi)
+        r = Ragged.from_lengths(lens, [0] * len(lens))
+        io = _unmask_io(lens, conf, masked, argmax, tokens, tau)
+        eb_unmask_select_lps(r, io["conf"], io["argmax"], io["tau"],
+                             torch.from_numpy(p_psi).cuda(), tau_psi, io["masked"], io["tokens"],
+                             io["unmask"], io["n_commit"], io["resolved"])
+        _assert_same(_outputs(io), ref)
+
+
+@pytest.mark.parametrize("m", [0, 1, 3, 40, 5000])
+def test_unmask_topm_random_ragged(m):
+    say(f"unmask topm m={m}")
+    rng = np.random.default_rng(24 + m)
+    lens, conf, masked, argmax, tokens, tau = _random_blocks(rng, 25, 300, tie_grid=10)
+    lens[3] = 2600                                  # a block longer than one rank-count round
+    lens[4] = 0
+    T = sum(lens)
+    conf = (rng.integers(0, 10, T) / 10.0).astype(np.float32)
+    masked = (rng.random(T) < 0.6).astype(np.uint8)
+    argmax = rng.integers(0, 1000, T).astype(np.int32)
+    tokens = np.where(masked == 1, -1, 5).astype(np.int32)
+    if m > 0:
+        tau = np.full(len(lens), 2.0, np.float32)    # budget only
+        tau[::3] = 0.8                              # threshold and budget together
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    ref = oracle.unmask_select_topm(conf, argmax, masked, tokens, tau, cu, m)
+    r = Ragged.from_lengths(lens, [0] * len(lens))
+    io = _unmask_io(lens, conf, masked, argmax, tokens, tau)
+    eb_unmask_select_topm(r, io["conf"], io["argmax"], io["tau"], m, io["masked"], io["tokens"],
+                          io["unmask"], io["n_commit"], io["resolved"])
+    _assert_same(_outputs(io), ref)
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_lps_path_workload(name):
+    """LM head with the gap, LPS features and the union accept rule on a named workload, in the
+    launch configuration of a whole batch; the oracle on sampled blocks."""
+    say(f"lps path workload={name}")
+    case = make_step(name)
+    full = case.T <= 64
+    nonempty = np.flatnonzero(case.block_lens > 0)
+    blocks = nonempty.tolist() if full else sorted({int(nonempty[0]), int(nonempty[-1]),
+                                                    int(nonempty[len(nonempty) // 2])})
+    enforce_margins(case, blocks)
+    dt, T, B = case.dtype, case.T, case.batch
+    ds = DeviceStep(case)
+    gap = _features_run(ds, T)
+    feat = torch.empty((T, 4), device="cuda")
+    pos = torch.empty(T, device="cuda")
+    rho = torch.empty(B, device="cuda")
+    eb_lps_features(ds.ragged, case.cfg.vocab, ds.conf, ds.entropy, torch.from_numpy(gap).cuda(),
+                    ds.masked, feat, pos, rho)
+    p_psi = router_scores(case.cfg.seed, "p_psi", T)
+    tau_psi = np.float32(0.9)
+    eb_unmask_select_lps(ds.ragged, ds.conf, ds.argmax, ds.tau, torch.from_numpy(p_psi).cuda(),
+                         tau_psi, ds.masked, ds.tokens, ds.unmask, ds.n_commit, ds.resolved)
+    torch.cuda.synchronize()
+    say("  gpu done")
+    rows = np.concatenate([np.arange(case.cu_block[b], case.cu_block[b + 1]) for b in blocks])
+    ref = oracle.lmhead_confidence(as_f32(case.h, dt), as_f32(case.w, dt), rows=rows)
+    np.testing.assert_array_equal(ds.argmax.cpu().numpy()[rows], ref["argmax"])
+    np.testing.assert_allclose(ds.conf.cpu().numpy()[rows], ref["conf"], rtol=0, atol=STAT_ATOL)
+    np.testing.assert_allclose(gap[rows], ref["top2_gap"], rtol=0, atol=STAT_ATOL)
+    sub_lens = [int(case.block_lens[b]) for b in blocks]
+    sub_cu = np.concatenate([[0], np.cumsum(sub_lens)]).astype(np.int32)
+    fref = oracle.lps_features(ref["conf"], ref["entropy"], ref["top2_gap"], case.masked[rows],
+                               sub_cu, case.cfg.vocab)
+    np.testing.assert_allclose(feat.cpu().numpy()[rows], fref["feat"], rtol=0, atol=STAT_ATOL)
+    np.testing.assert_allclose(pos.cpu().numpy()[rows], fref["pos"], rtol=0, atol=1e-6)
+    np.testing.assert_allclose(rho.cpu().numpy()[blocks], fref["mask_ratio"], rtol=0, atol=1e-6)
+    uref = oracle.unmask_select_lps(ref["conf"], ref["argmax"], case.masked[rows],
+                                    case.tokens[rows], case.tau[blocks], sub_cu, p_psi[rows],
+                                    tau_psi)
+    np.testing.assert_array_equal(ds.unmask.cpu().numpy()[rows], uref["unmask"])
+    np.testing.assert_array_equal(ds.tokens.cpu().numpy()[rows], uref["tokens"])
+    np.testing.assert_array_equal(ds.n_commit.cpu().numpy()[blocks], uref["n_commit"])
+    np.testing.assert_array_equal(ds.resolved.cpu().numpy()[blocks], uref["resolved"])
+    g = gap
+    c = ds.conf.cpu().numpy()
+    assert (g >= -1e-6).all() and (g <= c + 1e-6).all()

@@ -370,3 +370,15 @@ def custom_config(name: str = "custom", *, seed: int = 7, batch: int = 1, hq: in
     return StepConfig(name=name, seed=seed, batch=batch, hq=hq, hkv=hkv, head_dim=head_dim,
                       hidden=hidden, vocab=vocab, block_len=block_len, prefix_len=prefix_len,
                       run_max=run_max, mask=mask, taus=taus, dtype=dtype)
+
+
+# --------------------------------------------------------------------------------------------
+# Router-score stand-ins.  The LBS and LPS routers are trained networks (absent here); the
+# post-passes that consume their outputs take the scores as inputs.  These draws are uniform on
+# [0, 1) in float32 from their own counter-keyed streams, so they never shift the step's draws.
+# --------------------------------------------------------------------------------------------
+def router_scores(seed: int, stream: str, shape) -> np.ndarray:
+    """Seeded float32 scores on [0, 1), e.g. stream "p_psi" (one per block row) or "p_phi"."""
+    key = sum(ord(c) * 131 ** i for i, c in enumerate(stream)) % (2 ** 31)
+    rng = np.random.default_rng([seed, 7, key])
+    return rng.random(shape, dtype=np.float32)
