@@ -94,6 +94,32 @@ eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int he
                         size_t ws_bytes, eb_stream_t stream);
 
 /* ---------------------------------------------------------------------------------------
+ * Block attention with a dual cache (Sec. 6.3, Tab. 6): as eb_block_attn, with each
+ * sequence's keys extended by its cached suffix rows, the context right of the block,
+ *
+ *   keys of sequence b = prefix rows cu_prefix[b] .. cu_prefix[b+1]-1 of k_pre / v_pre
+ *                      + block rows  cu_block[b]  .. cu_block[b+1]-1  of k_blk / v_blk
+ *                      + suffix rows cu_suffix[b] .. cu_suffix[b+1]-1 of k_suf / v_suf
+ *
+ * (the keys form a set: the order of the segments does not change the result).
+ *   k_suf, v_suf [total_suffix, hkv, head_dim] of dtype dt; cu_suffix device [batch+1] int32,
+ *   non-decreasing from 0 to total_suffix; max_suffix its largest difference.
+ * ws: at least eb_block_attn_dual_workspace(...) bytes.
+ * ------------------------------------------------------------------------------------- */
+typedef struct {
+  int32_t total_suffix, max_suffix;
+  const int32_t* cu_suffix; /* device [batch+1] */
+} eb_suffix;
+
+size_t eb_block_attn_dual_workspace(eb_dtype dt, const eb_ragged* r, const eb_suffix* sfx, int hq,
+                                    int hkv, int head_dim);
+eb_status eb_block_attn_dual(eb_dtype dt, const eb_ragged* r, const eb_suffix* sfx, int hq,
+                             int hkv, int head_dim, float scale, const void* q, const void* k_blk,
+                             const void* v_blk, const void* k_pre, const void* v_pre,
+                             const void* k_suf, const void* v_suf, void* out, void* ws,
+                             size_t ws_bytes, eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
  * Fused LM head and confidence statistics (Alg. 5: softmax of the backbone logits, top-1
  * confidence and token; Eq. app-confidence; Sec. 5.1: entropy, normalised by ln|V| for the
  * block selector).  For each row i of h:
@@ -202,6 +228,30 @@ eb_status eb_unmask_select_topm(const eb_ragged* r, const float* conf, const int
                                 const float* tau, int32_t m, uint8_t* masked, int32_t* tokens,
                                 uint8_t* unmask, int32_t* n_commit, uint8_t* resolved,
                                 eb_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * LBS active-block selection post-pass (Sec. 5.1; Alg. 5, block selection) for each of n_seq
+ * sequences over a generation window of `window` positions.  With M the masked positions of
+ * sequence s (ascending):
+ *
+ *   if |M| <= l_min:  B = M                                               (size fallback)
+ *   else:  C = { i in M : p_phi[s, i] > 0.5 && x_hat[s, i] != eos_id }   (router, EOS removal)
+ *          B = C up to (not including) its first position whose distance to the previous
+ *              position of C exceeds g_max                                (max-gap filter)
+ *          if |B| < l_min:  B = the first l_b positions of M             (min-tokens fallback)
+ *
+ *   masked [n_seq, window] u8, p_phi [n_seq, window] f32 (the LBS router's probability; the
+ *   router itself is not part of this library), x_hat [n_seq, window] i32   (inputs)
+ *   block [n_seq, window] u8 (1 = in B), size [n_seq] i32 = |B|,
+ *   first [n_seq] i32 = smallest position of B or -1 when B is empty       (outputs)
+ *
+ * Distances are differences of positions (g_max = 1 keeps only contiguous runs).  Requires
+ * l_min, l_b >= 0 and g_max >= 1.  Integer-exact.
+ * ------------------------------------------------------------------------------------- */
+eb_status eb_lbs_select(int32_t n_seq, int32_t window, const uint8_t* masked,
+                        const float* p_phi, const int32_t* x_hat, int32_t eos_id, int32_t l_min,
+                        int32_t l_b, int32_t g_max, uint8_t* block, int32_t* size,
+                        int32_t* first, eb_stream_t stream);
 
 /* ---------------------------------------------------------------------------------------
  * One whole denoising step: eb_block_attn, then eb_lmhead_confidence over the T block rows

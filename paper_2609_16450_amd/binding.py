@@ -29,6 +29,11 @@ class eb_ragged(ctypes.Structure):
                 ("max_prefix", ctypes.c_int32), ("cu_block", _P), ("cu_prefix", _P)]
 
 
+class eb_suffix(ctypes.Structure):
+    _fields_ = [("total_suffix", ctypes.c_int32), ("max_suffix", ctypes.c_int32),
+                ("cu_suffix", _P)]
+
+
 class eb_step_trace(ctypes.Structure):
     _fields_ = [("attn_begin", _P), ("attn_end", _P), ("lmhead_begin", _P), ("lmhead_end", _P),
                 ("select_begin", _P), ("select_end", _P)]
@@ -53,6 +58,13 @@ EXPORTS = {
     "eb_block_attn": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(eb_ragged), ctypes.c_int,
                                      ctypes.c_int, ctypes.c_int, ctypes.c_float, _P, _P, _P, _P,
                                      _P, _P, _P, ctypes.c_size_t, _P]),
+    "eb_block_attn_dual_workspace": (ctypes.c_size_t, [ctypes.c_int, ctypes.POINTER(eb_ragged),
+                                                       ctypes.POINTER(eb_suffix), ctypes.c_int,
+                                                       ctypes.c_int, ctypes.c_int]),
+    "eb_block_attn_dual": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(eb_ragged),
+                                          ctypes.POINTER(eb_suffix), ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_int, ctypes.c_float, _P, _P, _P, _P, _P, _P,
+                                          _P, _P, _P, ctypes.c_size_t, _P]),
     "eb_lmhead_workspace": (ctypes.c_size_t, [ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                               ctypes.c_int]),
     "eb_lmhead_confidence": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -70,6 +82,9 @@ EXPORTS = {
                                             ctypes.c_float, _P, _P, _P, _P, _P, _P]),
     "eb_unmask_select_topm": (ctypes.c_int, [ctypes.POINTER(eb_ragged), _P, _P, _P,
                                              ctypes.c_int32, _P, _P, _P, _P, _P, _P]),
+    "eb_lbs_select": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, _P, _P, _P, ctypes.c_int32,
+                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, _P, _P,
+                                     _P]),
     "eb_decode_step_workspace": (ctypes.c_size_t, [ctypes.POINTER(eb_step_desc)]),
     "eb_decode_step": (ctypes.c_int, [ctypes.POINTER(eb_step_desc), _P, ctypes.c_size_t, _P]),
     "eb_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -237,6 +252,36 @@ def eb_block_attn(r: Ragged, q, k_blk, v_blk, k_pre, v_pre, out, scale: Optional
            "eb_block_attn")
 
 
+def eb_block_attn_dual(r: Ragged, cu_suffix: torch.Tensor, max_suffix: int, q, k_blk, v_blk,
+                       k_pre, v_pre, k_suf, v_suf, out, scale: Optional[float] = None,
+                       ws: Optional[torch.Tensor] = None, stream=None) -> None:
+    """out <- block attention over the prefix, block and cached suffix keys (eb.h)."""
+    dt = _dtype_code(q)
+    T, hq, D = q.shape
+    hkv = k_blk.shape[1]
+    U = k_suf.shape[0]
+    _dev(q, "q", q.dtype, (r.total_block, hq, D))
+    _dev(k_blk, "k_blk", q.dtype, (r.total_block, hkv, D))
+    _dev(v_blk, "v_blk", q.dtype, (r.total_block, hkv, D))
+    _dev(k_pre, "k_pre", q.dtype, (r.total_prefix, hkv, D))
+    _dev(v_pre, "v_pre", q.dtype, (r.total_prefix, hkv, D))
+    _dev(k_suf, "k_suf", q.dtype, (U, hkv, D))
+    _dev(v_suf, "v_suf", q.dtype, (U, hkv, D))
+    _dev(out, "out", q.dtype, (r.total_block, hq, D))
+    _dev(cu_suffix, "cu_suffix", torch.int32, (r.batch + 1,))
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    rc = r.c()
+    sc = eb_suffix(U, int(max_suffix), cu_suffix.data_ptr())
+    lib = load()
+    need = int(lib.eb_block_attn_dual_workspace(dt, ctypes.byref(rc), ctypes.byref(sc), hq, hkv, D))
+    wp, wn = _workspace(need, ws, q.device)
+    _check(lib.eb_block_attn_dual(dt, ctypes.byref(rc), ctypes.byref(sc), hq, hkv, D, scale,
+                                  q.data_ptr(), k_blk.data_ptr(), v_blk.data_ptr(),
+                                  k_pre.data_ptr(), v_pre.data_ptr(), k_suf.data_ptr(),
+                                  v_suf.data_ptr(), out.data_ptr(), wp, wn, _stream(stream)),
+           "eb_block_attn_dual")
+
+
 def eb_lmhead_workspace(dtype: int, n_rows: int, hidden: int, vocab: int) -> int:
     return int(load().eb_lmhead_workspace(dtype, n_rows, hidden, vocab))
 
@@ -363,6 +408,22 @@ def eb_unmask_select_topm(r: Ragged, conf, argmax, tau, m: int, masked, tokens, 
                                         tokens.data_ptr(), unmask.data_ptr(), n_commit.data_ptr(),
                                         resolved.data_ptr(), _stream(stream)),
            "eb_unmask_select_topm")
+
+
+def eb_lbs_select(masked, p_phi, x_hat, eos_id: int, l_min: int, l_b: int, g_max: int, block,
+                  size, first, stream=None) -> None:
+    """LBS active-block post-pass over [n_seq, window] windows (eb.h)."""
+    n, L = masked.shape
+    _dev(masked, "masked", torch.uint8, (n, L))
+    _dev(p_phi, "p_phi", torch.float32, (n, L))
+    _dev(x_hat, "x_hat", torch.int32, (n, L))
+    _dev(block, "block", torch.uint8, (n, L))
+    _dev(size, "size", torch.int32, (n,))
+    _dev(first, "first", torch.int32, (n,))
+    _check(load().eb_lbs_select(n, L, masked.data_ptr(), p_phi.data_ptr(), x_hat.data_ptr(),
+                                int(eos_id), int(l_min), int(l_b), int(g_max), block.data_ptr(),
+                                size.data_ptr(), first.data_ptr(), _stream(stream)),
+           "eb_lbs_select")
 
 
 class StepBuffers:

@@ -29,6 +29,11 @@ struct AttnParams {
   const uint16_t* k_pre;
   const uint16_t* v_pre;
   uint16_t* out;
+  // optional cached suffix segment (dual cache): rows cu_suffix[b] .. cu_suffix[b+1]-1 of
+  // k_suf / v_suf are further keys of sequence b; cu_suffix == nullptr: none
+  const int32_t* cu_suffix;
+  const uint16_t* k_suf;
+  const uint16_t* v_suf;
   // key split: keys of a sequence are cut into ranges of kps keys, one workgroup per range;
   // with nsplit > 1 the workgroups write unnormalised partials that attn_merge_kernel combines
   int nsplit, kps;
@@ -65,7 +70,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
   const int n_rows = len * G;
   const int row0 = blockIdx.x * kRowsPerWg;
   if (row0 >= n_rows) return;  // whole workgroup: this tile lies past the block
-  const int n_keys = plen + len;
+  const int sbeg = p.cu_suffix ? p.cu_suffix[b] : 0;
+  const int slen = p.cu_suffix ? p.cu_suffix[b + 1] - sbeg : 0;
+  const int n_keys = plen + len + slen;
   const int kbeg = sp * p.kps;
   if (kbeg >= n_keys) return;  // whole workgroup: this key range lies past the sequence
   const int kend = min(n_keys, kbeg + p.kps);
@@ -98,9 +105,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
   const int kp = tid & 31, dg = tid >> 5;
   constexpr int kVd = D / 8;
 
-  auto key_src = [&](int j, const uint16_t* pre, const uint16_t* blk) -> const uint16_t* {
+  // key j of the sequence: prefix rows, then block rows, then suffix rows (an unordered set)
+  auto key_src = [&](int j, const uint16_t* pre, const uint16_t* blk,
+                     const uint16_t* suf) -> const uint16_t* {
     if (j < plen) return pre + (static_cast<size_t>(pbeg + j) * p.hkv + g) * D;
-    return blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
+    if (j < plen + len) return blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
+    return suf + (static_cast<size_t>(sbeg + j - plen - len) * p.hkv + g) * D;
   };
 
   // Loads are unconditional with clamped key indices (a conditional load would be waited for
@@ -113,14 +123,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
       const int c = tid + i * kThreads;
       const int key = c / (D / 8), col = (c % (D / 8)) * 8;
       const int j = min(kv0 + key, kend - 1);
-      kreg[i] = *reinterpret_cast<const u32x4*>(key_src(j, p.k_pre, p.k_blk) + col);
+      kreg[i] = *reinterpret_cast<const u32x4*>(key_src(j, p.k_pre, p.k_blk, p.k_suf) + col);
     }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int j = min(kv0 + 2 * kp + e, kend - 1);
 #pragma unroll
       for (int c = 0; c < kVd / 8; ++c)
-        vreg[e][c] = *reinterpret_cast<const u32x4*>(key_src(j, p.v_pre, p.v_blk) + dg * kVd + 8 * c);
+        vreg[e][c] = *reinterpret_cast<const u32x4*>(key_src(j, p.v_pre, p.v_blk, p.v_suf) +
+                                                     dg * kVd + 8 * c);
     }
   };
   auto sstore = [&](int kv0) {
@@ -264,7 +275,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p, int total
     if (p.cu_block[mid] <= row) lo = mid; else hi = mid - 1;
   }
   const int b = lo;
-  const int n_keys = (p.cu_prefix[b + 1] - p.cu_prefix[b]) + (p.cu_block[b + 1] - p.cu_block[b]);
+  const int n_keys = (p.cu_prefix[b + 1] - p.cu_prefix[b]) + (p.cu_block[b + 1] - p.cu_block[b]) +
+                     (p.cu_suffix ? p.cu_suffix[b + 1] - p.cu_suffix[b] : 0);
   const int nvalid = min(p.nsplit, (n_keys + p.kps - 1) / p.kps);
   const size_t base = static_cast<size_t>(rh) * p.nsplit;
   float M = -INFINITY;
@@ -298,6 +310,9 @@ struct AttnParamsF32 {
   const float* k_pre;
   const float* v_pre;
   float* out;
+  const int32_t* cu_suffix;  // nullptr: no suffix segment
+  const float* k_suf;
+  const float* v_suf;
 };
 
 __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParamsF32 p) {
@@ -313,12 +328,27 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParamsF32 p) {
   const float* qr = p.q + (static_cast<size_t>(bbeg + i) * p.hq + h) * D;
   const float q0 = lane < D ? qr[lane] : 0.f;
   const float q1 = lane + 64 < D ? qr[lane + 64] : 0.f;
+  const int sbeg = p.cu_suffix ? p.cu_suffix[b] : 0;
+  const int slen = p.cu_suffix ? p.cu_suffix[b + 1] - sbeg : 0;
   float m = -INFINITY, l = 0.f, a0 = 0.f, a1 = 0.f;
-  for (int j = 0; j < plen + len; ++j) {
-    const float* kr = (j < plen) ? p.k_pre + (static_cast<size_t>(pbeg + j) * p.hkv + g) * D
-                                 : p.k_blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
-    const float* vr = (j < plen) ? p.v_pre + (static_cast<size_t>(pbeg + j) * p.hkv + g) * D
-                                 : p.v_blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
+  for (int j = 0; j < plen + len + slen; ++j) {
+    size_t off;
+    const float *kb, *vb;
+    if (j < plen) {
+      off = static_cast<size_t>(pbeg + j);
+      kb = p.k_pre;
+      vb = p.v_pre;
+    } else if (j < plen + len) {
+      off = static_cast<size_t>(bbeg + j - plen);
+      kb = p.k_blk;
+      vb = p.v_blk;
+    } else {
+      off = static_cast<size_t>(sbeg + j - plen - len);
+      kb = p.k_suf;
+      vb = p.v_suf;
+    }
+    const float* kr = kb + (off * p.hkv + g) * D;
+    const float* vr = vb + (off * p.hkv + g) * D;
     float dot = (lane < D ? q0 * kr[lane] : 0.f) + (lane + 64 < D ? q1 * kr[lane + 64] : 0.f);
     for (int mask = 32; mask >= 1; mask >>= 1) dot += __shfl_xor(dot, mask);
     const float sc = dot * p.scale;
@@ -342,11 +372,12 @@ struct SplitPlan {
   int nsplit, kps;
 };
 
-SplitPlan split_plan(int batch, int max_block, int max_prefix, int hq, int hkv) {
+// max_keys: the largest number of keys of a sequence (prefix + block + suffix).
+SplitPlan split_plan(int batch, int max_block, int max_keys, int hq, int hkv) {
   const int group = hq / hkv;
   const long row_tiles = (static_cast<long>(max_block) * group + kRowsPerWg - 1) / kRowsPerWg;
   const long base = row_tiles * hkv * batch;
-  const int stages = (max_prefix + max_block + kKeys - 1) / kKeys;
+  const int stages = (max_keys + kKeys - 1) / kKeys;
   int nsplit = static_cast<int>((kTargetWgs + base - 1) / base);
   nsplit = max(1, min(nsplit, stages));
   const int stages_per = (stages + nsplit - 1) / nsplit;
@@ -358,9 +389,9 @@ SplitPlan split_plan(int batch, int max_block, int max_prefix, int hq, int hkv) 
 }  // namespace
 
 size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_block, int max_block,
-                           int max_prefix, int hq, int hkv, int head_dim) {
+                           int max_keys, int hq, int hkv, int head_dim) {
   if (!bf16 || !allow_split || total_block == 0 || max_block == 0) return 0;
-  const SplitPlan sp = split_plan(batch, max_block, max_prefix, hq, hkv);
+  const SplitPlan sp = split_plan(batch, max_block, max_keys, hq, hkv);
   if (sp.nsplit == 1) return 0;
   return static_cast<size_t>(total_block) * hq * sp.nsplit * (head_dim + 2) * sizeof(float);
 }
@@ -368,16 +399,18 @@ size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_blo
 hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s) {
   if (a.total_block == 0 || a.max_block == 0) return hipSuccess;
   const int group = a.hq / a.hkv;
+  const int max_keys = a.max_prefix + a.max_block + (a.cu_suffix ? a.max_suffix : 0);
   if (!bf16) {
     AttnParamsF32 p{a.cu_block, a.cu_prefix, a.hq, a.hkv, group, a.head_dim, a.scale,
                     static_cast<const float*>(a.q), static_cast<const float*>(a.k_blk),
                     static_cast<const float*>(a.v_blk), static_cast<const float*>(a.k_pre),
-                    static_cast<const float*>(a.v_pre), static_cast<float*>(a.out)};
+                    static_cast<const float*>(a.v_pre), static_cast<float*>(a.out), a.cu_suffix,
+                    static_cast<const float*>(a.k_suf), static_cast<const float*>(a.v_suf)};
     hipLaunchKernelGGL(attn_f32_kernel, dim3(a.max_block, a.hq, a.batch), dim3(64), 0, s, p);
     return hipGetLastError();
   }
-  const SplitPlan sp = allow_split ? split_plan(a.batch, a.max_block, a.max_prefix, a.hq, a.hkv)
-                                   : SplitPlan{1, (a.max_prefix + a.max_block + kKeys - 1) / kKeys * kKeys};
+  const SplitPlan sp = allow_split ? split_plan(a.batch, a.max_block, max_keys, a.hq, a.hkv)
+                                   : SplitPlan{1, (max_keys + kKeys - 1) / kKeys * kKeys};
   const size_t n_part = static_cast<size_t>(a.total_block) * a.hq * sp.nsplit;
   float* o_part = static_cast<float*>(ws);
   float* m_part = sp.nsplit > 1 ? o_part + n_part * a.head_dim : nullptr;
@@ -385,7 +418,8 @@ hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, 
   AttnParams p{a.cu_block, a.cu_prefix, a.hq, a.hkv, group, a.scale * kLog2e,
                static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k_blk),
                static_cast<const uint16_t*>(a.v_blk), static_cast<const uint16_t*>(a.k_pre),
-               static_cast<const uint16_t*>(a.v_pre), static_cast<uint16_t*>(a.out),
+               static_cast<const uint16_t*>(a.v_pre), static_cast<uint16_t*>(a.out), a.cu_suffix,
+               static_cast<const uint16_t*>(a.k_suf), static_cast<const uint16_t*>(a.v_suf),
                sp.nsplit, sp.kps, sp.nsplit > 1 ? o_part : nullptr, m_part, l_part};
   const long rows = static_cast<long>(a.max_block) * group;
   dim3 grid(static_cast<unsigned>((rows + kRowsPerWg - 1) / kRowsPerWg), a.hkv,

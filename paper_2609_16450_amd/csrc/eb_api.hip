@@ -131,7 +131,8 @@ const char* eb_version(void) { return "libeb 0.1 (gfx950)"; }
 size_t eb_block_attn_workspace(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim) {
   if (!r || r->batch < 1 || hq < 1 || hkv < 1 || hq % hkv || r->total_block <= 0) return 0;
   return round_up(eb::block_attn_ws_bytes(dt == EB_BF16, true, r->batch, r->total_block,
-                                          r->max_block, r->max_prefix, hq, hkv, head_dim));
+                                          r->max_block, r->max_prefix + r->max_block, hq, hkv,
+                                          head_dim));
 }
 
 eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim,
@@ -147,6 +148,41 @@ eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int he
                  r->cu_block, r->cu_prefix, hq, hkv, head_dim, scale, q, k_blk, v_blk,
                  k_pre, v_pre, out};
   return hip_status(eb::block_attn(dt == EB_BF16, true, a, ws, stream), "eb_block_attn launch");
+}
+
+size_t eb_block_attn_dual_workspace(eb_dtype dt, const eb_ragged* r, const eb_suffix* sfx, int hq,
+                                    int hkv, int head_dim) {
+  if (!r || !sfx || r->batch < 1 || hq < 1 || hkv < 1 || hq % hkv || r->total_block <= 0 ||
+      sfx->max_suffix < 0)
+    return 0;
+  return round_up(eb::block_attn_ws_bytes(dt == EB_BF16, true, r->batch, r->total_block,
+                                          r->max_block,
+                                          r->max_prefix + r->max_block + sfx->max_suffix, hq,
+                                          hkv, head_dim));
+}
+
+eb_status eb_block_attn_dual(eb_dtype dt, const eb_ragged* r, const eb_suffix* sfx, int hq,
+                             int hkv, int head_dim, float scale, const void* q, const void* k_blk,
+                             const void* v_blk, const void* k_pre, const void* v_pre,
+                             const void* k_suf, const void* v_suf, void* out, void* ws,
+                             size_t ws_bytes, eb_stream_t stream) {
+  eb_status st = check_attn(dt, r, hq, hkv, head_dim, scale, q, k_blk, v_blk, k_pre, v_pre, out);
+  if (st != EB_OK) return st;
+  if (!sfx) return fail(EB_ERR_INVALID, "suffix descriptor is NULL");
+  if (sfx->total_suffix < 0 || sfx->max_suffix < 0 || !sfx->cu_suffix)
+    return fail(EB_ERR_INVALID, "need total_suffix, max_suffix >= 0 and cu_suffix");
+  if (sfx->total_suffix > 0 && (!k_suf || !v_suf))
+    return fail(EB_ERR_INVALID, "NULL k_suf / v_suf with total_suffix > 0");
+  if (dt == EB_BF16 && ((k_suf && !aligned16(k_suf)) || (v_suf && !aligned16(v_suf))))
+    return fail(EB_ERR_INVALID, "bf16 tensors must be 16-byte aligned");
+  const size_t need = eb_block_attn_dual_workspace(dt, r, sfx, hq, hkv, head_dim);
+  if (ws_bytes < need || (need && !ws))
+    return fail(EB_ERR_WORKSPACE, "attention workspace %zu bytes < required %zu", ws_bytes, need);
+  eb::AttnArgs a{r->batch, r->total_block, r->max_block, r->total_prefix, r->max_prefix,
+                 r->cu_block, r->cu_prefix, hq, hkv, head_dim, scale, q, k_blk, v_blk,
+                 k_pre, v_pre, out, sfx->max_suffix, sfx->cu_suffix, k_suf, v_suf};
+  return hip_status(eb::block_attn(dt == EB_BF16, true, a, ws, stream),
+                    "eb_block_attn_dual launch");
 }
 
 size_t eb_lmhead_workspace(eb_dtype dt, int n_rows, int hidden, int vocab) {
@@ -249,6 +285,24 @@ eb_status eb_unmask_select(const eb_ragged* r, const float* conf, const int32_t*
   return hip_status(eb::unmask_select(r->batch, r->max_block, r->cu_block, conf, argmax, tau,
                                       masked, tokens, unmask, n_commit, resolved, stream),
                     "eb_unmask_select launch");
+}
+
+eb_status eb_lbs_select(int32_t n_seq, int32_t window, const uint8_t* masked,
+                        const float* p_phi, const int32_t* x_hat, int32_t eos_id, int32_t l_min,
+                        int32_t l_b, int32_t g_max, uint8_t* block, int32_t* size,
+                        int32_t* first, eb_stream_t stream) {
+  if (n_seq < 0 || window < 0)
+    return fail(EB_ERR_INVALID, "need n_seq, window >= 0 (got %d, %d)", n_seq, window);
+  if (l_min < 0 || l_b < 0 || g_max < 1)
+    return fail(EB_ERR_INVALID, "need l_min, l_b >= 0 and g_max >= 1 (got %d, %d, %d)", l_min,
+                l_b, g_max);
+  if (n_seq == 0) return ok();
+  if (!size || !first) return fail(EB_ERR_INVALID, "NULL size / first");
+  if (window > 0 && (!masked || !p_phi || !x_hat || !block))
+    return fail(EB_ERR_INVALID, "NULL masked / p_phi / x_hat / block");
+  return hip_status(eb::lbs_select(n_seq, window, masked, p_phi, x_hat, eos_id, l_min, l_b, g_max,
+                                   block, size, first, stream),
+                    "eb_lbs_select launch");
 }
 
 size_t eb_decode_step_workspace(const eb_step_desc* d) {

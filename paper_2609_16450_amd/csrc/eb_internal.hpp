@@ -30,11 +30,17 @@ struct AttnArgs {
   float scale;
   const void *q, *k_blk, *v_blk, *k_pre, *v_pre;
   void* out;
+  // optional cached suffix segment (dual cache); cu_suffix == nullptr: none
+  int max_suffix = 0;
+  const int32_t* cu_suffix = nullptr;
+  const void* k_suf = nullptr;
+  const void* v_suf = nullptr;
 };
 // Workspace for key-split partials (0 when the launch needs no split).  Without allow_split
-// one workgroup covers all keys of its query tile and no workspace is used.
+// one workgroup covers all keys of its query tile and no workspace is used.  max_keys is the
+// largest number of keys of a sequence (prefix + block + suffix).
 size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_block,
-                           int max_block, int max_prefix, int hq, int hkv, int head_dim);
+                           int max_block, int max_keys, int hq, int hkv, int head_dim);
 hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s);
 
 // ---- unmask ---------------------------------------------------------------------------
@@ -53,5 +59,10 @@ hipError_t unmask_select_topm(int batch, const int32_t* cu_block, const float* c
 hipError_t lps_features(int batch, const int32_t* cu_block, int vocab, const float* conf,
                         const float* entropy, const float* gap, const uint8_t* masked,
                         float* feat, float* pos, float* mask_ratio, hipStream_t s);
+
+// ---- LBS post-pass ----------------------------------------------------------------------
+hipError_t lbs_select(int n_seq, int window, const uint8_t* masked, const float* p_phi,
+                      const int32_t* x_hat, int eos, int l_min, int l_b, int g_max,
+                      uint8_t* block, int32_t* size, int32_t* first, hipStream_t s);
 
 }  // namespace eb

@@ -92,6 +92,18 @@ def test_next_row_entry_points_reject_bad_arguments():
     assert lib.eb_unmask_select_topm(ctypes.byref(r), 0x100, 0x100, 0x100, -1, *([0x100] * 5),
                                      None) == B.EB_ERR_INVALID
     assert "m must be" in B.eb_last_error()
+    # LBS post-pass: g_max >= 1, outputs required
+    assert lib.eb_lbs_select(2, 16, *([0x100] * 3), 1, 2, 32, 0, *([0x100] * 3), None) == \
+        B.EB_ERR_INVALID
+    assert lib.eb_lbs_select(2, 16, *([0x100] * 3), 1, 2, 32, 5, 0x100, None, 0x100, None) == \
+        B.EB_ERR_INVALID
+    # dual cache: descriptor required, suffix pointers required when it has rows
+    assert lib.eb_block_attn_dual(B.EB_BF16, ctypes.byref(r), None, 4, 4, 128, 0.1,
+                                  *([0x100] * 8), None, 0, None) == B.EB_ERR_INVALID
+    sfx = B.eb_suffix(10, 10, 0x3000)
+    assert lib.eb_block_attn_dual(B.EB_BF16, ctypes.byref(r), ctypes.byref(sfx), 4, 4, 128, 0.1,
+                                  *([0x100] * 5), None, None, 0x100, None, 0, None) == \
+        B.EB_ERR_INVALID
 
 
 def test_workspace_queries():

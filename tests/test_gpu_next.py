@@ -240,3 +240,130 @@ def test_lps_path_workload(name):
     g = gap
     c = ds.conf.cpu().numpy()
     assert (g >= -1e-6).all() and (g <= c + 1e-6).all()
+
+
+# --------------------------------------------------------------------------------------
+# dual-cache attention (a cached suffix segment as further keys)
+# --------------------------------------------------------------------------------------
+from paper_2609_16450_amd import eb_block_attn, eb_block_attn_dual  # noqa: E402
+from workloads import suffix_segment  # noqa: E402
+
+DUAL_CASES = [
+    # batch, hq, hkv, D, block_len, prefix_len, suffix lens, dtype
+    (1, 4, 4, 64, ("fixed", 32), ("fixed", 96), [40], "f32"),
+    (3, 4, 2, 64, ("uniform", 0, 20), ("uniform", 0, 70), [0, 5, 33], "f32"),
+    (1, 32, 32, 128, ("fixed", 32), ("fixed", 512), [480], "bf16"),
+    (4, 8, 2, 128, ("uniform", 0, 40), ("uniform", 0, 200), [0, 65, 1, 130], "bf16"),
+    (3, 28, 4, 128, ("uniform", 10, 60), ("fixed", 300), [64, 0, 200], "bf16"),
+    (5, 4, 1, 64, ("choice", (1, 63, 64, 65, 129)), ("choice", (0, 1, 64)), [0, 1, 63, 64, 300], "bf16"),
+]
+
+
+@pytest.mark.parametrize("batch,hq,hkv,D,bl,pl,sl,dt", DUAL_CASES)
+def test_block_attn_dual(batch, hq, hkv, D, bl, pl, sl, dt):
+    say(f"dual attn batch={batch} hq={hq} hkv={hkv} D={D} suffix={sl} dtype={dt}")
+    cfg = custom_config(seed=500 + batch * hq, batch=batch, hq=hq, hkv=hkv, head_dim=D,
+                        block_len=bl, prefix_len=pl, hidden=64, vocab=64, dtype=dt)
+    case = make_step(cfg)
+    if case.T == 0:
+        pytest.skip("all blocks empty")
+    cu_s, k_s, v_s = suffix_segment(cfg.seed, sl, hkv, D, dt)
+    f = {k: as_f32(getattr(case, k), dt) for k in ("q", "k_blk", "v_blk", "k_pre", "v_pre")}
+    ref = oracle.block_attention(**f, cu_block=case.cu_block, cu_prefix=case.cu_prefix, hq=hq,
+                                 hkv=hkv, k_suf=as_f32(k_s, dt), v_suf=as_f32(v_s, dt),
+                                 cu_suffix=cu_s)
+    ds = DeviceStep(case)
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    to_dev = lambda a: (torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if dt == "bf16"
+                        else torch.from_numpy(a)).cuda()
+    eb_block_attn_dual(ds.ragged, torch.from_numpy(cu_s).cuda(), max(sl), ds.q, ds.k_blk,
+                       ds.v_blk, ds.k_pre, ds.v_pre, to_dev(k_s), to_dev(v_s), ds.attn_out)
+    torch.cuda.synchronize()
+    got = ds.attn_out.float().cpu().numpy()
+    tol = dict(rtol=2e-2, atol=2e-2) if dt == "bf16" else dict(rtol=1e-4, atol=1e-4)
+    np.testing.assert_allclose(got, ref, **tol)
+    # an all-empty suffix gives exactly the prefix-cache result
+    zero = np.zeros(batch + 1, np.int32)
+    out2 = torch.empty_like(ds.attn_out)
+    eb_block_attn_dual(ds.ragged, torch.from_numpy(zero).cuda(), 0, ds.q, ds.k_blk, ds.v_blk,
+                       ds.k_pre, ds.v_pre, to_dev(k_s[:0]), to_dev(v_s[:0]), out2)
+    eb_block_attn(ds.ragged, ds.q, ds.k_blk, ds.v_blk, ds.k_pre, ds.v_pre, ds.attn_out)
+    torch.cuda.synchronize()
+    assert torch.equal(out2.view(torch.uint8) if dt == "bf16" else out2,
+                       ds.attn_out.view(torch.uint8) if dt == "bf16" else ds.attn_out)
+    assert tdt == ds.q.dtype
+
+
+def test_block_attn_dual_workload_b16():
+    """llada8b_b16 shapes (16 sequences, block 64, prefix 1024, 32 heads x 128) with a cached
+    suffix of 512 rows per sequence; the oracle on three sampled sequences."""
+    say("dual attn workload llada8b_b16 + suffix 512")
+    case = make_step("llada8b_b16")
+    cfg = case.cfg
+    sl = [512] * case.batch
+    cu_s, k_s, v_s = suffix_segment(cfg.seed, sl, cfg.hkv, cfg.head_dim, "bf16")
+    ds = DeviceStep(case)
+    to_dev = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    eb_block_attn_dual(ds.ragged, torch.from_numpy(cu_s).cuda(), 512, ds.q, ds.k_blk, ds.v_blk,
+                       ds.k_pre, ds.v_pre, to_dev(k_s), to_dev(v_s), ds.attn_out)
+    torch.cuda.synchronize()
+    got = ds.attn_out.float().cpu().numpy()
+    for b in (0, 7, 15):
+        rows = np.arange(case.cu_block[b], case.cu_block[b + 1])
+        prow = np.arange(case.cu_prefix[b], case.cu_prefix[b + 1])
+        srow = np.arange(cu_s[b], cu_s[b + 1])
+        f = lambda a: as_f32(a, "bf16")
+        one = lambda n: np.array([0, n], np.int32)
+        ref = oracle.block_attention(f(case.q[rows]), f(case.k_blk[rows]), f(case.v_blk[rows]),
+                                     f(case.k_pre[prow]), f(case.v_pre[prow]), one(rows.size),
+                                     one(prow.size), cfg.hq, cfg.hkv, k_suf=f(k_s[srow]),
+                                     v_suf=f(v_s[srow]), cu_suffix=one(srow.size))
+        np.testing.assert_allclose(got[rows], ref, rtol=2e-2, atol=2e-2)
+
+
+# --------------------------------------------------------------------------------------
+# LBS block-selection post-pass
+# --------------------------------------------------------------------------------------
+from paper_2609_16450_amd import eb_lbs_select  # noqa: E402
+from workloads import lbs_window  # noqa: E402
+
+
+def _lbs_gpu(masked, p_phi, x_hat, eos, l_min, l_b, g_max):
+    n, L = masked.shape
+    d = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    block = torch.full((n, L), 7, dtype=torch.uint8, device="cuda")
+    size = torch.full((n,), -9, dtype=torch.int32, device="cuda")
+    first = torch.full((n,), -9, dtype=torch.int32, device="cuda")
+    eb_lbs_select(d(masked), d(p_phi), d(x_hat), eos, l_min, l_b, g_max, block, size, first)
+    torch.cuda.synchronize()
+    return dict(block=block.cpu().numpy(), size=size.cpu().numpy(), first=first.cpu().numpy())
+
+
+def _lbs_compare(masked, p_phi, x_hat, eos, l_min, l_b, g_max):
+    ref = oracle.lbs_select(masked, p_phi, x_hat, eos, l_min, l_b, g_max)
+    got = _lbs_gpu(masked, p_phi, x_hat, eos, l_min, l_b, g_max)
+    for k in ("block", "size", "first"):
+        np.testing.assert_array_equal(got[k], ref[k], err_msg=k)
+
+
+def test_lbs_random_windows():
+    say("lbs random windows")
+    rng = np.random.default_rng(31)
+    for it in range(30):
+        n = int(rng.integers(1, 20))
+        L = int(rng.choice([1, 7, 64, 255, 256, 257, 700, 2049]))
+        masked = (rng.random((n, L)) < rng.random()).astype(np.uint8)
+        p_phi = rng.choice(np.array([0.1, 0.5, 0.5000001, 0.9], np.float32), (n, L))
+        x_hat = rng.integers(0, 5, (n, L)).astype(np.int32)
+        l_min, l_b, g_max = int(rng.integers(0, 40)), int(rng.integers(0, 64)), int(rng.integers(1, 8))
+        _lbs_compare(masked, p_phi, x_hat, 4, l_min, l_b, g_max)
+
+
+@pytest.mark.parametrize("window", [512, 4096])
+def test_lbs_generation_window(window):
+    # 64 sequences over a generation window (512 as in App. F), min size 4, fallback 32,
+    # max gap 5 (the values given for the block-forward setting keep g_max = 5 by default)
+    say(f"lbs window={window}")
+    masked, p_phi, x_hat = lbs_window(2024, 64, window, 126464, 126081)
+    for l_min, l_b, g_max in ((4, 32, 5), (16, 32, 1), (200, 32, 3)):
+        _lbs_compare(masked, p_phi, x_hat, 126081, l_min, l_b, g_max)

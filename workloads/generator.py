@@ -222,7 +222,8 @@ def _cu(lens: np.ndarray) -> np.ndarray:
 
 
 _CHUNK = 1 << 22          # elements per independent normal stream chunk
-_STREAM = {"q": 1, "k_blk": 2, "v_blk": 3, "k_pre": 4, "v_pre": 5, "w": 6, "h_noise": 7}
+_STREAM = {"q": 1, "k_blk": 2, "v_blk": 3, "k_pre": 4, "v_pre": 5, "w": 6, "h_noise": 7,
+           "k_suf": 8, "v_suf": 9}
 
 
 def _threads() -> int:
@@ -382,3 +383,37 @@ def router_scores(seed: int, stream: str, shape) -> np.ndarray:
     key = sum(ord(c) * 131 ** i for i, c in enumerate(stream)) % (2 ** 31)
     rng = np.random.default_rng([seed, 7, key])
     return rng.random(shape, dtype=np.float32)
+
+
+def suffix_segment(seed: int, suffix_lens, hkv: int, head_dim: int, dtype: str):
+    """Seeded cached-suffix keys/values (the context right of the block, for dual-cache
+    attention): N(0, 1) entries in the storage dtype from their own streams.  Returns
+    (cu_suffix int32 [B+1], k_suf, v_suf [U, hkv, head_dim])."""
+    lens = np.asarray(suffix_lens, dtype=np.int64)
+    cu = _cu(lens)
+    U = int(cu[-1])
+    k = _normal_stream(seed, "k_suf", (U, hkv, head_dim), 1.0, dtype)
+    v = _normal_stream(seed, "v_suf", (U, hkv, head_dim), 1.0, dtype)
+    return cu, k, v
+
+
+def lbs_window(seed: int, n_seq: int, window: int, vocab: int, eos_id: int):
+    """Seeded inputs of the LBS post-pass over a generation window: per sequence a decoding
+    progress f ~ U[0, 1] (positions left of f * window mostly committed, masked fraction 0.9
+    to the right), router probabilities p_phi from router_scores, and predicted tokens that are
+    uniform ids except an EOS tail (from a per-sequence start in the last 40% of the window),
+    where the predictions concentrate on EOS at the end of the response (App. H)."""
+    rng = np.random.default_rng([seed, 11])
+    masked = np.zeros((n_seq, window), dtype=np.uint8)
+    x_hat = rng.integers(0, vocab, (n_seq, window)).astype(np.int32)
+    x_hat[x_hat == eos_id] = (eos_id + 1) % vocab
+    pos = np.arange(window)
+    for s in range(n_seq):
+        f = rng.random()
+        left = rng.random(window) < 0.05
+        right = rng.random(window) < 0.9
+        masked[s] = np.where(pos < int(f * window), left, right).astype(np.uint8)
+        tail = int(window * (0.6 + 0.4 * rng.random()))
+        x_hat[s, tail:] = eos_id
+    p_phi = router_scores(seed, "p_phi", (n_seq, window))
+    return masked, p_phi, x_hat
