@@ -12,6 +12,7 @@ fp64 CPU oracle timed on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import math
@@ -19,6 +20,8 @@ import os
 import platform
 import sys
 import time
+
+import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -108,6 +111,146 @@ def cpu_baseline(case, budget_s: float = 15.0):
                       f"{t_total:.1f} s on {platform.processor() or platform.machine()}"}
 
 
+SUFFIX_LEN = 256         # cached suffix rows per sequence on the dual-cache leg
+LBS_WINDOW = 512         # generation window of the LBS leg (generation length 512, App. F)
+TAU_PSI = 0.9            # LPS acceptance threshold on the lps leg
+TOP_M = 2                # per-block budget on the topm leg
+
+
+def timed(torch, stream, steps, run):
+    """Milliseconds per call of run(i) over `steps` calls, host clock between synchronisations."""
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        run(i)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def variant_leg(args, torch, eb, case, copies, stream) -> int:
+    """The next-row paths: one JSON line with the same fields as the headline."""
+    from workloads import lbs_window, router_scores, suffix_segment
+
+    cfg, T, B = case.cfg, case.T, case.batch
+    dev = "cuda:0"
+    u8 = lambda n: torch.empty(max(n, 1), dtype=torch.uint8, device=dev)
+    bf = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dt_code = eb.EB_BF16 if cfg.dtype == "bf16" else eb.EB_F32
+    extra = []
+    for ds in copies:
+        x = {"attn_ws": u8(eb.eb_block_attn_workspace(dt_code, ds.ragged, cfg.hq, cfg.hkv,
+                                                       cfg.head_dim)),
+             "lm_ws": u8(eb.eb_lmhead_features_workspace(dt_code, T, cfg.hidden, cfg.vocab)),
+             "gap": torch.empty(T, device=dev), "feat": torch.empty((T, 4), device=dev),
+             "pos": torch.empty(T, device=dev), "rho": torch.empty(B, device=dev),
+             "p_psi": torch.from_numpy(router_scores(cfg.seed, "p_psi", T)).to(dev)}
+        if args.path == "dual":
+            cu_s, k_s, v_s = suffix_segment(cfg.seed, [SUFFIX_LEN] * B, cfg.hkv, cfg.head_dim,
+                                            cfg.dtype)
+            conv = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16)) \
+                if cfg.dtype == "bf16" else torch.from_numpy
+            x.update(cu_s=torch.from_numpy(cu_s).to(dev), k_s=conv(k_s).to(dev),
+                     v_s=conv(v_s).to(dev))
+            from paper_2609_16450_amd.binding import eb_suffix
+            x["attn_ws"] = u8(eb.load().eb_block_attn_dual_workspace(
+                dt_code, ctypes.byref(ds.ragged.c()),
+                ctypes.byref(eb_suffix(SUFFIX_LEN * B, SUFFIX_LEN, 0)), cfg.hq, cfg.hkv,
+                cfg.head_dim))
+        extra.append(x)
+    if args.path == "lbs":
+        m, p, xh = lbs_window(cfg.seed, B, LBS_WINDOW, cfg.vocab, cfg.vocab - 1)
+        lb = [dict(m=torch.from_numpy(m).to(dev), p=torch.from_numpy(p).to(dev),
+                   x=torch.from_numpy(xh).to(dev),
+                   block=torch.empty((B, LBS_WINDOW), dtype=torch.uint8, device=dev),
+                   size=torch.empty(B, dtype=torch.int32, device=dev),
+                   first=torch.empty(B, dtype=torch.int32, device=dev)) for _ in copies]
+
+    def run(i, lm_events=None):
+        ds, x = copies[i % len(copies)], extra[i % len(copies)]
+        if args.path == "lbs":
+            L = lb[i % len(copies)]
+            eb.eb_lbs_select(L["m"], L["p"], L["x"], cfg.vocab - 1, 4, 32, 5, L["block"],
+                             L["size"], L["first"], stream=stream)
+            return
+        if args.path == "dual":
+            eb.eb_block_attn_dual(ds.ragged, x["cu_s"], SUFFIX_LEN, ds.q, ds.k_blk, ds.v_blk,
+                                  ds.k_pre, ds.v_pre, x["k_s"], x["v_s"], ds.attn_out,
+                                  ws=x["attn_ws"], stream=stream)
+        else:
+            eb.eb_block_attn(ds.ragged, ds.q, ds.k_blk, ds.v_blk, ds.k_pre, ds.v_pre, ds.attn_out,
+                             ws=x["attn_ws"], stream=stream)
+        if lm_events:
+            lm_events[0].record(stream)
+        if args.path == "lps":
+            eb.eb_lmhead_features(ds.h, ds.w, ds.conf, ds.entropy, ds.argmax, x["gap"],
+                                  ds.max_logit, ws=x["lm_ws"], stream=stream)
+        else:
+            eb.eb_lmhead_confidence(ds.h, ds.w, ds.conf, ds.entropy, ds.argmax, ds.max_logit,
+                                    ws=x["lm_ws"], stream=stream)
+        if lm_events:
+            lm_events[1].record(stream)
+        if args.path == "lps":
+            eb.eb_lps_features(ds.ragged, cfg.vocab, ds.conf, ds.entropy, x["gap"], ds.masked,
+                               x["feat"], x["pos"], x["rho"], stream=stream)
+            eb.eb_unmask_select_lps(ds.ragged, ds.conf, ds.argmax, ds.tau, x["p_psi"], TAU_PSI,
+                                    ds.masked, ds.tokens, ds.unmask, ds.n_commit, ds.resolved,
+                                    stream=stream)
+        elif args.path == "topm":
+            eb.eb_unmask_select_topm(ds.ragged, ds.conf, ds.argmax, ds.tau, TOP_M, ds.masked,
+                                     ds.tokens, ds.unmask, ds.n_commit, ds.resolved,
+                                     stream=stream)
+        else:
+            eb.eb_unmask_select(ds.ragged, ds.conf, ds.argmax, ds.tau, ds.masked, ds.tokens,
+                                ds.unmask, ds.n_commit, ds.resolved, stream=stream)
+
+    for i in range(args.warmup):
+        run(i)
+    ms = timed(torch, stream, args.steps, run)
+    units = B * LBS_WINDOW if args.path == "lbs" else T
+    config = {"workload": cfg.name, "path": args.path, "batch": B, "block_positions": T,
+              "prefix_positions": case.S, "heads": f"{cfg.hq}/{cfg.hkv}x{cfg.head_dim}",
+              "hidden": cfg.hidden, "vocab": cfg.vocab, "input_copies": len(copies)}
+    if args.path == "lbs":
+        nbytes = units * (1 + 4 + 4 + 1) + 8 * B   # masked, p_phi, x_hat in; block, size, first out
+        roof = {"bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "traffic": None, "kernel": "lbs_select_kernel", "kernel_us": ms * 1e3,
+                "algorithmic_bytes": nbytes, "algorithmic_flops": 0.0}
+        config.update(window=LBS_WINDOW, l_min=4, l_b=32, g_max=5)
+        metric, unit = "generation-window positions selected/sec (LBS post-pass)", "positions/s"
+    else:
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for i, pair in enumerate(evs):
+            run(i, pair)
+        torch.cuda.synchronize()
+        lm_ms = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+        nbytes, flops = lmhead_work(cfg, T)
+        if cfg.dtype == "f32":
+            bound, peak, unit_r, achieved = "alu", MFMA_F32_PEAK_TFLOPS, "TFLOP/s", flops / (lm_ms * 1e-3) / 1e12
+        elif flops / nbytes < (MFMA_BF16_PEAK_TFLOPS * 1e12) / (HBM_PEAK_GBS * 1e9):
+            bound, peak, unit_r, achieved = "hbm", HBM_PEAK_GBS, "GB/s", nbytes / (lm_ms * 1e-3) / 1e9
+        else:
+            bound, peak, unit_r, achieved = "mfma", MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", flops / (lm_ms * 1e-3) / 1e12
+        roof = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit_r,
+                "frac": achieved / peak, "traffic": None,
+                "kernel": lmhead_kernel_name(cfg.dtype, T) + " + lmhead_combine_kernel",
+                "kernel_us": lm_ms * 1e3, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+        if args.path == "dual":
+            config["suffix_positions"] = SUFFIX_LEN * B
+        if args.path == "lps":
+            config["tau_psi"] = TAU_PSI
+        if args.path == "topm":
+            config["m"] = TOP_M
+        metric, unit = METRIC, "positions/s"
+    print(json.dumps({"metric": metric, "value": units / (ms * 1e-3), "unit": unit, "n_gpus": 1,
+                      "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+                      "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+                      "dtype": cfg.dtype, "data": "synthetic", "config": config,
+                      "roofline": roof}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -118,6 +261,11 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 3 device-to-device copies of BYTES (calibrates HBM counters)")
+    ap.add_argument("--path", default="step", choices=["step", "lps", "topm", "dual", "lbs"],
+                    help="step: eb_decode_step (the headline); lps: attention + LM head with the "
+                         "top-2 gap + LPS features + union accept rule; topm: attention + LM head "
+                         "+ top-m commit; dual: dual-cache attention + LM head + unmask; lbs: the "
+                         "LBS post-pass over a 512-position generation window per sequence")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -152,6 +300,9 @@ def main() -> int:
     copies = [DeviceStep(case, device="cuda:0") for _ in range(max(1, args.copies))]
     stream = torch.cuda.current_stream()
     log(f"bench: T={T} S={case.S} warmup={args.warmup} steps={args.steps}")
+
+    if args.path != "step":
+        return variant_leg(args, torch, eb, case, copies, stream)
 
     def run(i, trace=None):
         ds = copies[i % len(copies)]

@@ -175,7 +175,7 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
       for (int r = 0; r < 4; ++r) {
         const int v = wb + tm * 16 + 4 * grp + r;
         const float z = acc[tm][nt][r];
-        if (kTop2 && v < we) m2 = fmaxf(m2, fminf(m, z));
+        if (kTop2 && v < we) m2 = __builtin_amdgcn_fmed3f(m, m2, z);
         if (v < we && z > m) {
           m = z;
           idx = v;
@@ -384,7 +384,8 @@ __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], i
       const int v = vbase + tm * 32 + 8 * (r >> 2) + (r & 3);
       if (full || v < vocab) {
         const float z = acc[tm][tn][r];
-        if (kTop2) mc2[r & 3] = fmaxf(mc2[r & 3], fminf(mc[r & 3], z));
+        // with mc >= mc2, the new second-largest is the median of (mc, mc2, z): one v_med3
+        if (kTop2) mc2[r & 3] = __builtin_amdgcn_fmed3f(mc[r & 3], mc2[r & 3], z);
         mc[r & 3] = fmaxf(mc[r & 3], z);
       }
     }
