@@ -21,7 +21,9 @@ namespace {
 // compute unit owns a contiguous slice of vocabulary rows.  Each of its 8 waves streams its
 // share of the slice from HBM straight into MFMA A-operand registers, keeping kDepth k-steps of
 // loads in flight; h, the B operand shared by all waves, goes through a double-buffered LDS
-// chunk.  Every W byte is read once, by one lane, with no LDS round trip.
+// chunk.  Every W byte is read once, by one lane, with no LDS round trip.  (Loading h per wave
+// straight into registers instead, with no LDS and no barrier, measured 237 us against 203 us
+// at 32 positions: the per-wave h traffic from L2 costs more than the shared chunks.)
 // ---------------------------------------------------------------------------------------
 constexpr int kStreamWaves = 8;
 constexpr int kStreamThreads = kStreamWaves * 64;
