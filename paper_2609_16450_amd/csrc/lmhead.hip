@@ -18,15 +18,13 @@ namespace {
 // Streaming kernel for few block positions (n_rows <= 32 * NT).
 //
 // With a handful of positions the product is a bandwidth-bound pass over W.  One workgroup per
-// compute unit owns a contiguous slice of vocabulary rows.  Each of its 8 waves streams its
-// share of the slice from HBM straight into MFMA A-operand registers, keeping kDepth k-steps of
-// loads in flight; h, the B operand shared by all waves, goes through a double-buffered LDS
+// compute unit owns a contiguous slice of vocabulary rows.  Each of its 16 waves (8 for slices
+// above 768 rows) streams its share of the slice from HBM straight into MFMA A-operand registers,
+// keeping kDepth k-steps of loads in flight; h, the B operand shared by all waves, goes through a double-buffered LDS
 // chunk.  Every W byte is read once, by one lane, with no LDS round trip.  (Loading h per wave
 // straight into registers instead, with no LDS and no barrier, measured 237 us against 203 us
 // at 32 positions: the per-wave h traffic from L2 costs more than the shared chunks.)
 // ---------------------------------------------------------------------------------------
-constexpr int kStreamWaves = 8;
-constexpr int kStreamThreads = kStreamWaves * 64;
 #ifndef EB_STREAM_GROUPS
 #define EB_STREAM_GROUPS 256
 #endif
@@ -54,8 +52,9 @@ __device__ __forceinline__ float top2_shfl_merge(float m, float m2, int mask) {
 }
 
 // kTop2: also track the second-largest logit of each (row, slice) into part2.
-template <int TM, int NT, int kDepth, bool kTop2>  // TM 16-row tiles per wave, NT 16-position tiles
-__global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
+// kWaves waves per workgroup, TM 16-row tiles per wave, NT 16-position tiles.
+template <int kWaves, int TM, int NT, int kDepth, bool kTop2>
+__global__ __launch_bounds__(kWaves * 64) void lmhead_stream16_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
     int vocab, int rows_per_wg, Partial* __restrict__ part, float* __restrict__ part2,
     int n_slices) {
@@ -64,8 +63,9 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
   constexpr int kSpc = KC / 32;        // k-steps per chunk
   constexpr int kHRows = NT * 16;
   constexpr int kHChunks16 = kHRows * KC / 8;
-  constexpr int kHPer = kHChunks16 / kStreamThreads;
-  static_assert(kHChunks16 % kStreamThreads == 0, "h chunk splits evenly");
+  constexpr int kThreads = kWaves * 64;
+  constexpr int kHPer = kHChunks16 / kThreads;
+  static_assert(kHChunks16 % kThreads == 0, "h chunk splits evenly");
   static_assert(kSpc % kDepth == 0, "chunk boundary falls on a group boundary");
   __shared__ __attribute__((aligned(16))) uint16_t hs[2][kHRows * kPitch];
 
@@ -74,7 +74,7 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
   const int wg = blockIdx.x;
   const int vb = wg * rows_per_wg;
   const int ve = min(vocab, vb + rows_per_wg);
-  const int rw = (rows_per_wg + kStreamWaves - 1) / kStreamWaves;
+  const int rw = (rows_per_wg + kWaves - 1) / kWaves;
   const int wb = vb + wave * rw;
   const int we = min(ve, wb + rw);
 
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
   auto load_h = [&](int c) {
 #pragma unroll
     for (int i = 0; i < kHPer; ++i) {
-      const int idx = tid + i * kStreamThreads;
+      const int idx = tid + i * kThreads;
       const int row = min(idx / (KC / 8), n_rows - 1);
       const int col = min(c * KC + (idx % (KC / 8)) * 8, hidden - 8);
       hreg[i] = *reinterpret_cast<const u32x4*>(h + static_cast<size_t>(row) * hidden + col);
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
   auto store_h = [&](int b, int c) {
 #pragma unroll
     for (int i = 0; i < kHPer; ++i) {
-      const int idx = tid + i * kStreamThreads;
+      const int idx = tid + i * kThreads;
       const int row = idx / (KC / 8), col = (idx % (KC / 8)) * 8;
       const bool ok = c * KC + col < hidden;
       *reinterpret_cast<u32x4*>(&hs[b][row * kPitch + col]) = ok ? hreg[i] : u32x4{0u, 0u, 0u, 0u};
@@ -164,9 +164,9 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
   for (int j = 0; j < kDepth; ++j) consume(nsteps_p - kDepth, j);
 
   __syncthreads();
-  Partial* red = reinterpret_cast<Partial*>(&hs[0][0]);  // [kStreamWaves][kHRows]
-  float* red2 = reinterpret_cast<float*>(red + kStreamWaves * kHRows);
-  static_assert(kStreamWaves * kHRows * (sizeof(Partial) + 4) <= sizeof(hs), "reduction fits");
+  Partial* red = reinterpret_cast<Partial*>(&hs[0][0]);  // [kWaves][kHRows]
+  float* red2 = reinterpret_cast<float*>(red + kWaves * kHRows);
+  static_assert(kWaves * kHRows * (sizeof(Partial) + 4) <= sizeof(hs), "reduction fits");
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     float m = kNegBig, m2 = kNegBig;
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
     Partial p = red[tid];
     float m2 = kTop2 ? red2[tid] : kNegBig;
 #pragma unroll
-    for (int k = 1; k < kStreamWaves; ++k) {
+    for (int k = 1; k < kWaves; ++k) {
       const Partial q = red[k * kHRows + tid];
       if (kTop2) m2 = top2_merge(p.m, m2, q.m, red2[k * kHRows + tid]);
       p = partial_merge(p, q);
@@ -221,43 +221,57 @@ __global__ __launch_bounds__(kStreamThreads) void lmhead_stream16_kernel(
   }
 }
 
-// k-steps of W loads in flight per wave (measured on MI355X; the macro exists so that other
-// settings can be built and timed).
+// k-steps of W loads in flight per wave with 16 waves (measured on MI355X; the macro exists so
+// that other settings can be built and timed).
 #ifndef EB_STREAM_DEPTH
-#define EB_STREAM_DEPTH 2
+#define EB_STREAM_DEPTH 8
 #endif
 constexpr int kStreamShape = 16;  // rows (and positions) per MFMA tile
 constexpr int kStreamDepth = EB_STREAM_DEPTH;
+// 16 waves per workgroup while each wave's share of the slice fits in kStreamMaxTm16 row tiles
+// (at 1024 threads a lane has 128 VGPRs; four tiles with two or more position tiles spill), else
+// 8 waves, which leaves 256 VGPRs per lane for up to 8 row tiles (16 waves with depth 8 measured
+// 186 us against 195 us for 8 waves with depth 2 at 32 positions of a 126464 x 4096 head).
+constexpr int kStreamMaxTm16 = 3;
+constexpr int kStreamMaxTm8 = 8;
 
 struct StreamPlan {
-  int groups, rows_per_wg, tm;  // tm: MFMA row tiles per wave
+  int groups, rows_per_wg, waves, tm;  // tm: MFMA row tiles per wave
 };
 
 StreamPlan stream_plan(int vocab) {
   const int groups = min(kStreamGroups, (vocab + 31) / 32);
   const int rows = (vocab + groups - 1) / groups;
-  const int rw = (rows + kStreamWaves - 1) / kStreamWaves;
-  return StreamPlan{groups, rows, (rw + kStreamShape - 1) / kStreamShape};
+  auto tiles = [&](int waves) {
+    const int rw = (rows + waves - 1) / waves;
+    return (rw + kStreamShape - 1) / kStreamShape;
+  };
+  if (tiles(16) <= kStreamMaxTm16) return StreamPlan{groups, rows, 16, tiles(16)};
+  return StreamPlan{groups, rows, 8, tiles(8)};
 }
 
 constexpr int kStreamMaxRows = 64;  // n_rows handled by the streaming kernel
-constexpr int kStreamMaxTm = 8;
 
 bool use_stream(int n_rows, int vocab) {
   if (n_rows > kStreamMaxRows) return false;
-  const int tm = stream_plan(vocab).tm;
-  if (n_rows > 2 * kStreamShape) return tm <= 6;  // register budget with four position tiles
-  return tm <= kStreamMaxTm;
+  const StreamPlan pl = stream_plan(vocab);
+  if (pl.waves == 16) return true;
+  if (n_rows > 2 * kStreamShape) return pl.tm <= 6;  // register budget with four position tiles
+  return pl.tm <= kStreamMaxTm8;
 }
 
-template <int TM, int NT, bool kTop2>
+template <int kWaves, int TM, int NT, bool kTop2>
 hipError_t launch_stream_tm(int n_rows, int hidden, int vocab, const StreamPlan& pl,
                             const void* h, const void* w, Partial* part, float* part2,
                             hipStream_t s) {
-  constexpr int D = (kStreamDepth * TM > 16) ? (16 / TM > 0 ? 16 / TM : 1) : kStreamDepth;
-  constexpr int Dp = D >= 4 ? 4 : (D >= 2 ? 2 : 1);  // divides the per-chunk step count
-  hipLaunchKernelGGL((lmhead_stream16_kernel<TM, NT, Dp, kTop2>), dim3(pl.groups),
-                     dim3(kStreamThreads), 0, s, static_cast<const uint16_t*>(h),
+  // 16 waves: up to 16 W registers in flight per lane (16 bytes each; 8 with four position
+  // tiles), at most kStreamDepth k-steps.  8 waves: two k-steps (more measured no faster).
+  constexpr int kBudget = kWaves == 8 ? 2 * TM : (NT >= 4 ? 8 : 16);
+  constexpr int D0 = kBudget / TM >= 1 ? kBudget / TM : 1;
+  constexpr int D = (kWaves == 16 && D0 > kStreamDepth) ? kStreamDepth : D0;
+  constexpr int Dp = D >= 8 ? 8 : (D >= 4 ? 4 : (D >= 2 ? 2 : 1));  // divides the per-chunk step count
+  hipLaunchKernelGGL((lmhead_stream16_kernel<kWaves, TM, NT, Dp, kTop2>), dim3(pl.groups),
+                     dim3(kWaves * 64), 0, s, static_cast<const uint16_t*>(h),
                      static_cast<const uint16_t*>(w), n_rows, hidden, vocab, pl.rows_per_wg, part,
                      part2, pl.groups);
   return hipGetLastError();
@@ -268,20 +282,23 @@ template <int NT, bool kTop2>
 hipError_t launch_stream(int n_rows, int hidden, int vocab, const void* h, const void* w,
                          Partial* part, float* part2, hipStream_t s) {
   const StreamPlan pl = stream_plan(vocab);
+  if (pl.waves == 16) {
+    switch (pl.tm) {
+      case 1: return launch_stream_tm<16, 1, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+      case 2: return launch_stream_tm<16, 2, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+      case 3: return launch_stream_tm<16, 3, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+      default: return hipErrorInvalidValue;  // excluded by stream_plan
+    }
+  }
+  // More than 48 tiles of rows per workgroup: the 8-wave shape has 7 or 8 tiles per wave.
   switch (pl.tm) {
-    case 1: return launch_stream_tm<1, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
-    case 2: return launch_stream_tm<2, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
-    case 3: return launch_stream_tm<3, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
-    case 4: return launch_stream_tm<4, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
-    case 5: return launch_stream_tm<5, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
-    case 6: return launch_stream_tm<6, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
     case 7:
       if constexpr (NT < 4)
-        return launch_stream_tm<7, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+        return launch_stream_tm<8, 7, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
       return hipErrorInvalidValue;
     case 8:
       if constexpr (NT < 4)
-        return launch_stream_tm<8, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+        return launch_stream_tm<8, 8, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
       return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;  // excluded by use_stream
   }

@@ -62,11 +62,12 @@ LM_CASES = [
     # large-batch kernel: several row tiles, vocabulary bands with a partial last band
     (600, 192, 9000, "bf16"),
     (300, 128, 1100, "bf16"),
-    # streaming kernel: 1..4 row tiles per wave, partial h chunks
+    # streaming kernel: 16 waves with 1..3 row tiles each, 8 waves with 7 or 8, partial h chunks
     (32, 256, 126464, "bf16"),
     (17, 128, 152064, "bf16"),
     (48, 192, 152064, "bf16"),
     (8, 64, 200000, "bf16"),
+    (2, 64, 262144, "bf16"),
     (40, 1600, 9000, "bf16"),
     (3, 4160, 20000, "bf16"),
     (32, 256, 2048, "f32"),
