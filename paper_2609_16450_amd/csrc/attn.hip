@@ -8,6 +8,7 @@
 // bf16 path: scores are computed transposed, S^T = K Q^T, so each lane owns one query row
 // (an MFMA column) and reduces its softmax statistics in registers; the probabilities then
 // feed P V directly as the B operand of O^T = V^T P^T, with V staged transposed in LDS.
+#include "attn_common.hpp"
 #include "eb_common.hpp"
 #include "eb_internal.hpp"
 
@@ -15,32 +16,9 @@ namespace eb {
 namespace {
 
 constexpr int kThreads = 256;   // 4 waves
-constexpr int kRowsPerWg = 128; // query rows (position, head-in-group) per workgroup
-constexpr int kKeys = 64;       // keys per LDS stage
+constexpr int kRowsPerWg = kAttnRowsPerWg;
+constexpr int kKeys = kAttnKeys;
 
-struct AttnParams {
-  const int32_t* cu_block;
-  const int32_t* cu_prefix;
-  int hq, hkv, group;
-  float scale_log2;  // scale * log2(e)
-  const uint16_t* q;
-  const uint16_t* k_blk;
-  const uint16_t* v_blk;
-  const uint16_t* k_pre;
-  const uint16_t* v_pre;
-  uint16_t* out;
-  // optional cached suffix segment (dual cache): rows cu_suffix[b] .. cu_suffix[b+1]-1 of
-  // k_suf / v_suf are further keys of sequence b; cu_suffix == nullptr: none
-  const int32_t* cu_suffix;
-  const uint16_t* k_suf;
-  const uint16_t* v_suf;
-  // key split: keys of a sequence are cut into ranges of kps keys, one workgroup per range;
-  // with nsplit > 1 the workgroups write unnormalised partials that attn_merge_kernel combines
-  int nsplit, kps;
-  float* o_part;  // [T * hq * nsplit, D]
-  float* m_part;  // [T * hq * nsplit]  running max (log2 units)
-  float* l_part;  // [T * hq * nsplit]  sum of 2^(s - m)
-};
 
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
   return static_cast<uint32_t>(f32_to_bf16_bits_rne(lo)) |
@@ -260,41 +238,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
     }
 }
 
-// Combine the key-split partials of each (block row, query head): one wavefront per pair,
-// splits merged in index order (max, rescale, sum), output rounded to bf16.
+// Combine the key-split partials of each (block row, query head), one wavefront per pair.
 template <int D>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p, int total_block) {
-  const int lane = threadIdx.x & 63;
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p, int total_block, int batch) {
   const int rh = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (rh >= total_block * p.hq) return;  // uniform per wavefront
-  const int row = rh / p.hq;
-  // sequence of this row: largest b with cu_block[b] <= row (blocks are non-empty here)
-  int lo = 0, hi = static_cast<int>(gridDim.y) - 1;  // gridDim.y carries the batch size
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (p.cu_block[mid] <= row) lo = mid; else hi = mid - 1;
-  }
-  const int b = lo;
-  const int n_keys = (p.cu_prefix[b + 1] - p.cu_prefix[b]) + (p.cu_block[b + 1] - p.cu_block[b]) +
-                     (p.cu_suffix ? p.cu_suffix[b + 1] - p.cu_suffix[b] : 0);
-  const int nvalid = min(p.nsplit, (n_keys + p.kps - 1) / p.kps);
-  const size_t base = static_cast<size_t>(rh) * p.nsplit;
-  float M = -INFINITY;
-  for (int k = 0; k < nvalid; ++k) M = fmaxf(M, p.m_part[base + k]);
-  constexpr int kPer = D / 64;  // values per lane
-  float acc[kPer] = {};
-  float L = 0.f;
-  for (int k = 0; k < nvalid; ++k) {
-    const float f = fast_exp2(p.m_part[base + k] - M);
-    L += f * p.l_part[base + k];
-    const float* o = p.o_part + (base + k) * D + lane * kPer;
-#pragma unroll
-    for (int e = 0; e < kPer; ++e) acc[e] += f * o[e];
-  }
-  const float inv = 1.0f / L;
-  uint16_t* dst = p.out + static_cast<size_t>(rh) * D + lane * kPer;
-#pragma unroll
-  for (int e = 0; e < kPer; ++e) dst[e] = f32_to_bf16_bits_rne(acc[e] * inv);
+  attn_merge_pair<D>(p, rh, batch, threadIdx.x & 63);
 }
 
 // fp32 path (small shapes): one wavefront per (block row, query head); lanes split the head
@@ -365,27 +314,6 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParamsF32 p) {
   if (lane + 64 < D) dst[lane + 64] = a1 / l;
 }
 
-// Key-split plan: enough workgroups to fill the chip (kTargetWgs), in whole 64-key stages.
-constexpr int kTargetWgs = 512;
-
-struct SplitPlan {
-  int nsplit, kps;
-};
-
-// max_keys: the largest number of keys of a sequence (prefix + block + suffix).
-SplitPlan split_plan(int batch, int max_block, int max_keys, int hq, int hkv) {
-  const int group = hq / hkv;
-  const long row_tiles = (static_cast<long>(max_block) * group + kRowsPerWg - 1) / kRowsPerWg;
-  const long base = row_tiles * hkv * batch;
-  const int stages = (max_keys + kKeys - 1) / kKeys;
-  int nsplit = static_cast<int>((kTargetWgs + base - 1) / base);
-  nsplit = max(1, min(nsplit, stages));
-  const int stages_per = (stages + nsplit - 1) / nsplit;
-  const int kps = stages_per * kKeys;
-  nsplit = (stages * kKeys + kps - 1) / kps;
-  return SplitPlan{nsplit, kps};
-}
-
 }  // namespace
 
 size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_block, int max_block,
@@ -396,10 +324,11 @@ size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_blo
   return static_cast<size_t>(total_block) * hq * sp.nsplit * (head_dim + 2) * sizeof(float);
 }
 
-hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s) {
+hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s,
+                      bool defer_merge) {
   if (a.total_block == 0 || a.max_block == 0) return hipSuccess;
   const int group = a.hq / a.hkv;
-  const int max_keys = a.max_prefix + a.max_block + (a.cu_suffix ? a.max_suffix : 0);
+  const int max_keys = attn_max_keys(a);
   if (!bf16) {
     AttnParamsF32 p{a.cu_block, a.cu_prefix, a.hq, a.hkv, group, a.head_dim, a.scale,
                     static_cast<const float*>(a.q), static_cast<const float*>(a.k_blk),
@@ -411,16 +340,7 @@ hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, 
   }
   const SplitPlan sp = allow_split ? split_plan(a.batch, a.max_block, max_keys, a.hq, a.hkv)
                                    : SplitPlan{1, (max_keys + kKeys - 1) / kKeys * kKeys};
-  const size_t n_part = static_cast<size_t>(a.total_block) * a.hq * sp.nsplit;
-  float* o_part = static_cast<float*>(ws);
-  float* m_part = sp.nsplit > 1 ? o_part + n_part * a.head_dim : nullptr;
-  float* l_part = sp.nsplit > 1 ? m_part + n_part : nullptr;
-  AttnParams p{a.cu_block, a.cu_prefix, a.hq, a.hkv, group, a.scale * kLog2e,
-               static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k_blk),
-               static_cast<const uint16_t*>(a.v_blk), static_cast<const uint16_t*>(a.k_pre),
-               static_cast<const uint16_t*>(a.v_pre), static_cast<uint16_t*>(a.out), a.cu_suffix,
-               static_cast<const uint16_t*>(a.k_suf), static_cast<const uint16_t*>(a.v_suf),
-               sp.nsplit, sp.kps, sp.nsplit > 1 ? o_part : nullptr, m_part, l_part};
+  const AttnParams p = attn_params(a, sp, ws);
   const long rows = static_cast<long>(a.max_block) * group;
   dim3 grid(static_cast<unsigned>((rows + kRowsPerWg - 1) / kRowsPerWg), a.hkv,
             static_cast<unsigned>(a.batch) * sp.nsplit);
@@ -429,13 +349,13 @@ hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, 
   else
     hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kThreads), 0, s, p);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || sp.nsplit == 1) return e;
+  if (e != hipSuccess || sp.nsplit == 1 || defer_merge) return e;
   const long pairs = static_cast<long>(a.total_block) * a.hq;
-  dim3 mgrid(static_cast<unsigned>((pairs + 3) / 4), static_cast<unsigned>(a.batch));
+  dim3 mgrid(static_cast<unsigned>((pairs + 3) / 4));
   if (a.head_dim == 128)
-    hipLaunchKernelGGL(attn_merge_kernel<128>, mgrid, dim3(256), 0, s, p, a.total_block);
+    hipLaunchKernelGGL(attn_merge_kernel<128>, mgrid, dim3(256), 0, s, p, a.total_block, a.batch);
   else
-    hipLaunchKernelGGL(attn_merge_kernel<64>, mgrid, dim3(256), 0, s, p, a.total_block);
+    hipLaunchKernelGGL(attn_merge_kernel<64>, mgrid, dim3(256), 0, s, p, a.total_block, a.batch);
   return hipGetLastError();
 }
 

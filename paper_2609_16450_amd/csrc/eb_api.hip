@@ -339,9 +339,13 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
                  d->v_blk, d->k_pre, d->v_pre, d->attn_out};
   const size_t attn_ws = eb_block_attn_workspace(d->dtype, r, d->hq, d->hkv, d->head_dim);
   char* lm_ws = static_cast<char*>(ws) + attn_ws;
+  // One epilogue launch (attention split merge + row statistics + unmask) when one workgroup
+  // can reduce a block's LM-head partials; otherwise the three kernels run one after another.
+  const int n_slices = T > 0 ? eb::lmhead_num_slices(bf16, T, d->vocab) : 0;
+  const bool fuse = eb::step_finish_fusable(r->max_block, n_slices);
 
   hipError_t e = tr ? mark(tr->attn_begin) : hipSuccess;
-  if (e == hipSuccess) e = eb::block_attn(bf16, true, a, ws, stream);
+  if (e == hipSuccess) e = eb::block_attn(bf16, true, a, ws, stream, fuse);
   if (e == hipSuccess && tr) e = mark(tr->attn_end);
   if (e != hipSuccess) return hip_status(e, "step attention launch");
 
@@ -351,12 +355,19 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
   if (e == hipSuccess && tr) e = mark(tr->lmhead_end);
   if (e != hipSuccess) return hip_status(e, "step LM-head launch");
   if (tr) e = mark(tr->select_begin);
-  if (e == hipSuccess && T > 0)
-    e = eb::lmhead_combine(bf16, T, d->vocab, lm_ws, d->conf, d->entropy_nats, d->argmax,
-                           d->max_logit, nullptr, stream);
-  if (e == hipSuccess)
-    e = eb::unmask_select(r->batch, r->max_block, r->cu_block, d->conf, d->argmax, d->tau,
-                          d->masked, d->tokens, d->unmask, d->n_commit, d->resolved, stream);
+  if (fuse) {
+    if (e == hipSuccess)
+      e = eb::step_finish(bf16, a, ws, T, d->vocab, lm_ws, d->conf, d->entropy_nats, d->argmax,
+                          d->max_logit, d->tau, d->masked, d->tokens, d->unmask, d->n_commit,
+                          d->resolved, stream);
+  } else {
+    if (e == hipSuccess && T > 0)
+      e = eb::lmhead_combine(bf16, T, d->vocab, lm_ws, d->conf, d->entropy_nats, d->argmax,
+                             d->max_logit, nullptr, stream);
+    if (e == hipSuccess)
+      e = eb::unmask_select(r->batch, r->max_block, r->cu_block, d->conf, d->argmax, d->tau,
+                            d->masked, d->tokens, d->unmask, d->n_commit, d->resolved, stream);
+  }
   if (e == hipSuccess && tr) e = mark(tr->select_end);
   return hip_status(e, "step select launch");
 }

@@ -84,10 +84,32 @@ __device__ __forceinline__ Partial partial_xor_merge(const Partial& p, int mask,
   return (lane & mask) ? partial_merge(q, p) : partial_merge(p, q);
 }
 
+// Reduction of one partial per lane to the wavefront's partial, returned on every lane: the
+// maximum M and the lowest index attaining it by max / min butterflies, then each lane's partial
+// rescaled to M (s 2^d and 2^d (t + s d) with d = (m - M) log2 e, the partial_merge formulas)
+// and s, t summed by a butterfly.  Each lane's sums use the same additions in the same order
+// (a + b on one lane, b + a on its partner), so every lane ends with identical bits.
+__device__ __forceinline__ Partial wave_finish(const Partial& acc) {
+  float M = acc.m;
+  for (int mask = 32; mask >= 1; mask >>= 1) M = fmaxf(M, __shfl_xor(M, mask));
+  int32_t idx = acc.m == M ? acc.idx : kNoIndex;
+  for (int mask = 32; mask >= 1; mask >>= 1) idx = min(idx, __shfl_xor(idx, mask));
+  const float d = fmaxf((acc.m - M) * kLog2e, -1.0e30f);  // empty lane: 2^d = 0
+  const float f = fast_exp2(d);
+  float s = acc.s * f;
+  float t = f * (acc.t + acc.s * d);
+  for (int mask = 32; mask >= 1; mask >>= 1) {
+    s += __shfl_xor(s, mask);
+    t += __shfl_xor(t, mask);
+  }
+  return Partial{M, s, t, idx};
+}
+
 // Merge of n partials p[0..n) by one wavefront in a fixed order: lane l merges p[l], p[l+64],
-// ... in index order, then a canonical butterfly; every lane ends with the same result.  Loads
-// are issued kBatch at a time, unconditionally (clamped index, masked merge), so that their
-// latencies overlap.
+// ... in index order, then wave_finish; every lane ends with the same result.  Loads are issued
+// kBatch at a time, unconditionally (clamped index), so that their latencies overlap; a lane
+// past the end merges an empty partial, which leaves its partial unchanged exactly (m and idx
+// kept, s + 0 * 0, t + 0), so the code has no branch.
 template <int kBatch = 4>
 __device__ __forceinline__ Partial wave_merge(const Partial* __restrict__ p, int n, int lane) {
   Partial acc = partial_empty();
@@ -97,10 +119,20 @@ __device__ __forceinline__ Partial wave_merge(const Partial* __restrict__ p, int
     for (int j = 0; j < kBatch; ++j) q[j] = p[min(base + 64 * j + lane, n - 1)];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j)
-      if (base + 64 * j + lane < n) acc = partial_merge(acc, q[j]);
+      acc = partial_merge(acc, base + 64 * j + lane < n ? q[j] : partial_empty());
   }
-  for (int mask = 32; mask >= 1; mask >>= 1) acc = partial_xor_merge(acc, mask, lane);
-  return acc;
+  return wave_finish(acc);
+}
+
+// Per-row outputs from a row's merged partial p: conf = 1 / s (the top-1 probability),
+// entropy in nats = ln s - ln 2 * t / s, argmax, and the top logit (max_logit optional).
+__device__ __forceinline__ void write_row_stats(const Partial& p, int row, float* conf,
+                                                float* entropy, int32_t* argmax,
+                                                float* max_logit) {
+  conf[row] = 1.0f / p.s;
+  entropy[row] = logf(p.s) - kLn2 * p.t / p.s;
+  argmax[row] = p.idx;
+  if (max_logit) max_logit[row] = p.m;
 }
 
 }  // namespace eb

@@ -41,7 +41,9 @@ struct AttnArgs {
 // largest number of keys of a sequence (prefix + block + suffix).
 size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_block,
                            int max_block, int max_keys, int hq, int hkv, int head_dim);
-hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s);
+// With defer_merge a key-split launch leaves its partials in ws for step_finish to merge.
+hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s,
+                      bool defer_merge = false);
 
 // ---- unmask ---------------------------------------------------------------------------
 hipError_t unmask_select(int batch, int max_block, const int32_t* cu_block, const float* conf,
@@ -59,6 +61,18 @@ hipError_t unmask_select_topm(int batch, const int32_t* cu_block, const float* c
 hipError_t lps_features(int batch, const int32_t* cu_block, int vocab, const float* conf,
                         const float* entropy, const float* gap, const uint8_t* masked,
                         float* feat, float* pos, float* mask_ratio, hipStream_t s);
+
+// ---- fused step epilogue ---------------------------------------------------------------
+// One launch after block_attn(..., defer_merge = true) and lmhead_partials: merges the attention
+// key splits, combines each row's LM-head partials into conf / entropy / argmax / max_logit,
+// and applies the threshold unmask per block.  Usable when one workgroup can reduce a block's
+// partials (max_block * n_slices <= kFinishMaxPartials).
+constexpr long kFinishMaxPartials = 1L << 16;
+bool step_finish_fusable(int max_block, int n_slices);
+hipError_t step_finish(bool bf16, const AttnArgs& a, void* attn_ws, int n_rows, int vocab,
+                       const void* lm_ws, float* conf, float* entropy, int32_t* argmax,
+                       float* max_logit, const float* tau, uint8_t* masked, int32_t* tokens,
+                       uint8_t* unmask, int32_t* n_commit, uint8_t* resolved, hipStream_t s);
 
 // ---- LBS post-pass ----------------------------------------------------------------------
 hipError_t lbs_select(int n_seq, int window, const uint8_t* masked, const float* p_phi,

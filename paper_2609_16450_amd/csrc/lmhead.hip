@@ -856,13 +856,9 @@ __global__ __launch_bounds__(256) void lmhead_combine_kernel(const Partial* __re
     }
   }
   if (lane == 0) {
-    const float inv = 1.0f / p.s;
-    conf[row] = inv;
-    entropy[row] = logf(p.s) - kLn2 * p.t / p.s;
-    argmax[row] = p.idx;
-    if (max_logit) max_logit[row] = p.m;
+    write_row_stats(p, row, conf, entropy, argmax, max_logit);
     // p_(1) - p_(2) = (1 - e^(z2 - m)) / s; 0 when the maximum is shared (z2 = m)
-    if (kTop2) top2_gap[row] = (1.0f - fast_exp2((m2 - p.m) * kLog2e)) * inv;
+    if (kTop2) top2_gap[row] = (1.0f - fast_exp2((m2 - p.m) * kLog2e)) * (1.0f / p.s);
   }
 }
 

@@ -300,3 +300,41 @@ def test_decode_step_is_deterministic():
     for a, b in zip(*outs):
         assert torch.equal(a.view(torch.uint8) if a.dtype == torch.bfloat16 else a,
                            b.view(torch.uint8) if b.dtype == torch.bfloat16 else b)
+
+
+# The step composes its kernels differently from the separate entry points (one epilogue launch
+# merges the attention key splits, reduces the LM-head partials and runs the unmask step), with
+# the same arithmetic, so every output must match them bit for bit.
+FUSE_CASES = [
+    # fused epilogue, attention key split merged there
+    ("llada8b_b1", None),
+    # fused, ragged blocks (some empty), GQA, large-batch LM kernel
+    ("ragged", dict(seed=31, batch=5, hq=8, hkv=2, head_dim=128, hidden=256, vocab=5000,
+                    block_len=("uniform", 0, 40), prefix_len=("uniform", 0, 300))),
+    # too many partials for one workgroup per block: separate kernels
+    ("long_block", dict(seed=32, batch=1, hq=2, hkv=2, head_dim=64, hidden=64, vocab=60000,
+                        block_len=("fixed", 300), prefix_len=("fixed", 64))),
+    # fp32 path
+    ("f32", dict(seed=33, batch=3, hq=4, hkv=2, head_dim=64, hidden=128, vocab=999,
+                 block_len=("uniform", 1, 20), prefix_len=("uniform", 0, 50), dtype="f32")),
+]
+
+
+@pytest.mark.parametrize("name,spec", FUSE_CASES, ids=[c[0] for c in FUSE_CASES])
+def test_decode_step_matches_separate_entry_points(name, spec):
+    say(f"decode_step vs separate entry points: {name}")
+    case = make_step(name if spec is None else custom_config(name, **spec))
+    a = DeviceStep(case)
+    eb_decode_step(a.buffers)
+    b = DeviceStep(case)
+    eb_block_attn(b.ragged, b.q, b.k_blk, b.v_blk, b.k_pre, b.v_pre, b.attn_out)
+    eb_lmhead_confidence(b.h, b.w, b.conf, b.entropy, b.argmax, b.max_logit)
+    eb_unmask_select(b.ragged, b.conf, b.argmax, b.tau, b.masked, b.tokens, b.unmask, b.n_commit,
+                     b.resolved)
+    torch.cuda.synchronize()
+    for field in ("attn_out", "conf", "entropy", "argmax", "max_logit", "tokens", "masked",
+                  "unmask", "n_commit", "resolved"):
+        x, y = getattr(a, field), getattr(b, field)
+        if x.dtype == torch.bfloat16:
+            x, y = x.view(torch.int16), y.view(torch.int16)
+        assert torch.equal(x, y), field
