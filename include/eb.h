@@ -254,8 +254,12 @@ eb_status eb_lbs_select(int32_t n_seq, int32_t window, const uint8_t* masked,
                         int32_t* first, eb_stream_t stream);
 
 /* ---------------------------------------------------------------------------------------
- * One whole denoising step: eb_block_attn, then eb_lmhead_confidence over the T block rows
- * of h, then eb_unmask_select, enqueued on `stream` with no host synchronisation.  The
+ * One whole denoising step (Alg. 5, one loop iteration): eb_block_attn, then
+ * eb_lmhead_confidence over the T block rows of h, then eb_unmask_select, enqueued on `stream`
+ * with no host synchronisation.  Every output equals, bit for bit, what those three calls
+ * produce; the step merely launches fewer kernels: the attention's key-split merge, the
+ * merge of the LM-head partials and the unmask run as one epilogue launch (unless a block's
+ * rows times the LM head's vocabulary slices exceed 65536, when they run separately).  The
  * workspace holds the attention's key-split partials followed by the LM-head partials.
  * Field meanings, layouts and requirements are those of the three calls above; the LM-head
  * rows are the block rows (n_rows = ragged.total_block).
@@ -265,9 +269,10 @@ eb_status eb_lbs_select(int32_t n_seq, int32_t window, const uint8_t* masked,
  * hipEventCreate); this times the kernels of one step without a host synchronisation.
  * ------------------------------------------------------------------------------------- */
 typedef struct {
-  eb_event_t attn_begin, attn_end;     /* around the attention kernel */
+  eb_event_t attn_begin, attn_end;     /* around the attention kernel (its split merge, if
+                                          any, runs in the epilogue) */
   eb_event_t lmhead_begin, lmhead_end; /* around the fused LM-head kernel (without its merge) */
-  eb_event_t select_begin, select_end; /* around the partial merge and the unmask kernels */
+  eb_event_t select_begin, select_end; /* around the epilogue: split merges and unmask */
 } eb_step_trace;
 
 typedef struct {

@@ -69,8 +69,9 @@ __global__ __launch_bounds__(kFinishThreads) void step_finish_kernel(
     }
   }
   __syncthreads();  // the block's conf / argmax rows are written before the block step reads them
-  unmask_block<kThreshold, kFinishThreads>(b, ap.cu_block, conf, argmax, tau, RuleArgs{nullptr, 0.f, 0}, masked,
-                           tokens, unmask, n_commit, resolved);
+  unmask_block<kThreshold, kFinishThreads>(b, ap.cu_block, conf, argmax, tau,
+                                           RuleArgs{nullptr, 0.f, 0}, masked, tokens, unmask,
+                                           n_commit, resolved);
 }
 
 }  // namespace
