@@ -192,7 +192,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
       for (int u = 0; u < 2; ++u) {
         u32x4 pb;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) pb[e] = pack2_bf16(sacc[kb][8 * u + 2 * e], sacc[kb][8 * u + 2 * e + 1]);
+        for (int e = 0; e < 4; ++e)
+          pb[e] = pack2_bf16(sacc[kb][8 * u + 2 * e], sacc[kb][8 * u + 2 * e + 1]);
         const bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
         const int kbase = kb * 32 + 16 * u + 4 * half;
 #pragma unroll

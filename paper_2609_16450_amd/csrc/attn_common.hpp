@@ -44,7 +44,8 @@ struct SplitPlan {
 // largest number of keys of a sequence (prefix + block + suffix).
 inline SplitPlan split_plan(int batch, int max_block, int max_keys, int hq, int hkv) {
   const int group = hq / hkv;
-  const long row_tiles = (static_cast<long>(max_block) * group + kAttnRowsPerWg - 1) / kAttnRowsPerWg;
+  const long row_tiles =
+      (static_cast<long>(max_block) * group + kAttnRowsPerWg - 1) / kAttnRowsPerWg;
   const long base = row_tiles * hkv * batch;
   const int stages = (max_keys + kAttnKeys - 1) / kAttnKeys;
   int nsplit = static_cast<int>((kAttnTargetWgs + base - 1) / base);

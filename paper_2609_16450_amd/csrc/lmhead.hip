@@ -19,11 +19,12 @@ namespace {
 //
 // With a handful of positions the product is a bandwidth-bound pass over W.  One workgroup per
 // compute unit owns a contiguous slice of vocabulary rows.  Each of its 16 waves (8 for slices
-// above 768 rows) streams its share of the slice from HBM straight into MFMA A-operand registers,
-// keeping kDepth k-steps of loads in flight; h, the B operand shared by all waves, goes through a double-buffered LDS
-// chunk.  Every W byte is read once, by one lane, with no LDS round trip.  (Loading h per wave
-// straight into registers instead, with no LDS and no barrier, measured 237 us against 203 us
-// at 32 positions: the per-wave h traffic from L2 costs more than the shared chunks.)
+// above 768 rows) streams its share of the slice from HBM straight into MFMA A-operand
+// registers, keeping kDepth k-steps of loads in flight; h, the B operand shared by all waves,
+// goes through a double-buffered LDS chunk.  Every W byte is read once, by one lane, with no
+// LDS round trip.  (Loading h per wave straight into registers instead, with no LDS and no
+// barrier, measured 237 us against 203 us at 32 positions: the per-wave h traffic from L2 costs
+// more than the shared chunks.)
 // ---------------------------------------------------------------------------------------
 #ifndef EB_STREAM_GROUPS
 #define EB_STREAM_GROUPS 256
@@ -269,7 +270,8 @@ hipError_t launch_stream_tm(int n_rows, int hidden, int vocab, const StreamPlan&
   constexpr int kBudget = kWaves == 8 ? 2 * TM : (NT >= 4 ? 8 : 16);
   constexpr int D0 = kBudget / TM >= 1 ? kBudget / TM : 1;
   constexpr int D = (kWaves == 16 && D0 > kStreamDepth) ? kStreamDepth : D0;
-  constexpr int Dp = D >= 8 ? 8 : (D >= 4 ? 4 : (D >= 2 ? 2 : 1));  // divides the per-chunk step count
+  // a power of two that divides the per-chunk step count
+  constexpr int Dp = D >= 8 ? 8 : (D >= 4 ? 4 : (D >= 2 ? 2 : 1));
   hipLaunchKernelGGL((lmhead_stream16_kernel<kWaves, TM, NT, Dp, kTop2>), dim3(pl.groups),
                      dim3(kWaves * 64), 0, s, static_cast<const uint16_t*>(h),
                      static_cast<const uint16_t*>(w), n_rows, hidden, vocab, pl.rows_per_wg, part,
@@ -284,9 +286,15 @@ hipError_t launch_stream(int n_rows, int hidden, int vocab, const void* h, const
   const StreamPlan pl = stream_plan(vocab);
   if (pl.waves == 16) {
     switch (pl.tm) {
-      case 1: return launch_stream_tm<16, 1, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
-      case 2: return launch_stream_tm<16, 2, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
-      case 3: return launch_stream_tm<16, 3, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+      case 1:
+        return launch_stream_tm<16, 1, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2,
+                                                    s);
+      case 2:
+        return launch_stream_tm<16, 2, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2,
+                                                    s);
+      case 3:
+        return launch_stream_tm<16, 3, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2,
+                                                    s);
       default: return hipErrorInvalidValue;  // excluded by stream_plan
     }
   }
