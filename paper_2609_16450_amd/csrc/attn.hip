@@ -20,9 +20,11 @@ constexpr int kRowsPerWg = kAttnRowsPerWg;
 constexpr int kKeys = kAttnKeys;
 
 
+// Two floats to two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32; lo in bits 0-15.
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
-  return static_cast<uint32_t>(f32_to_bf16_bits_rne(lo)) |
-         (static_cast<uint32_t>(f32_to_bf16_bits_rne(hi)) << 16);
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // Two workgroups per compute unit (<= 256 VGPRs per lane, no spills at D = 128), so one
@@ -112,26 +114,27 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
                                                      dg * kVd + 8 * c);
     }
   };
-  auto sstore = [&](int kv0) {
-    const u32x4 zero{0u, 0u, 0u, 0u};
+  // Keys past the end were loaded from a clamped (valid) row: finite values whose scores are
+  // masked to -inf below, so their probabilities are exactly 0 and they add nothing to O.
+  auto sstore = [&]() {
 #pragma unroll
     for (int i = 0; i < kKPer; ++i) {
       const int c = tid + i * kThreads;
       const int key = c / (D / 8), col = (c % (D / 8)) * 8;
-      *reinterpret_cast<u32x4*>(Ks + key * kKRow + col) = (kv0 + key < kend) ? kreg[i] : zero;
+      *reinterpret_cast<u32x4*>(Ks + key * kKRow + col) = kreg[i];
     }
-    const bool ok0 = kv0 + 2 * kp < kend, ok1 = kv0 + 2 * kp + 1 < kend;
+    // V^T: the 16-bit values of keys 2 kp and 2 kp + 1 at one d form one 32-bit word
 #pragma unroll
     for (int c = 0; c < kVd / 8; ++c)
 #pragma unroll
-      for (int w4 = 0; w4 < 4; ++w4)
-#pragma unroll
-        for (int hw = 0; hw < 2; ++hw) {
-          const int d = dg * kVd + 8 * c + 2 * w4 + hw;
-          const uint32_t lo = ok0 ? (vreg[0][c][w4] >> (16 * hw)) & 0xffffu : 0u;
-          const uint32_t hi = ok1 ? (vreg[1][c][w4] >> (16 * hw)) & 0xffffu : 0u;
-          *reinterpret_cast<uint32_t*>(Vt + d * kVRow + 2 * kp) = lo | (hi << 16);
-        }
+      for (int w4 = 0; w4 < 4; ++w4) {
+        const int d = dg * kVd + 8 * c + 2 * w4;
+        const uint32_t k0 = vreg[0][c][w4], k1 = vreg[1][c][w4];
+        *reinterpret_cast<uint32_t*>(Vt + d * kVRow + 2 * kp) =
+            __builtin_amdgcn_perm(k1, k0, 0x05040100u);  // low halves: value at d
+        *reinterpret_cast<uint32_t*>(Vt + (d + 1) * kVRow + 2 * kp) =
+            __builtin_amdgcn_perm(k1, k0, 0x07060302u);  // high halves: value at d + 1
+      }
   };
 
   const int n_stages = (kend - kbeg + kKeys - 1) / kKeys;
@@ -139,7 +142,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
   for (int st = 0; st < n_stages; ++st) {
     const int kv0 = kbeg + st * kKeys;
     __syncthreads();  // previous stage's LDS reads are done
-    sstore(kv0);
+    sstore();
     __syncthreads();
     if (st + 1 < n_stages) gload(kv0 + kKeys);
 
@@ -155,18 +158,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
         sacc[kb] = mfma32(kf, qf[s], sacc[kb]);
       }
     }
+    // raw scores; keys past the end (last stage only) masked to -inf
+    if (kv0 + kKeys > kend) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kv0 + kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          if (key >= kend) sacc[kb][r] = -INFINITY;
+        }
+    }
     float mloc = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kv0 + kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        const float x = (key < kend) ? sacc[kb][r] * p.scale_log2 : -INFINITY;
-        sacc[kb][r] = x;
-        mloc = fmaxf(mloc, x);
-      }
+      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sacc[kb][r]);
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-    const float m_new = fmaxf(m_run, mloc);
+    // scale > 0, so max(scale * s) = scale * max(s); e = 2^(scale s - m) with one FMA
+    const float m_new = fmaxf(m_run, mloc * p.scale_log2);
     const float alpha = fast_exp2(m_run - m_new);
     m_run = m_new;
     float lsum = 0.f;
@@ -174,15 +183,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = fast_exp2(sacc[kb][r] - m_new);
+        const float e = fast_exp2(fmaf(sacc[kb][r], p.scale_log2, -m_new));
         sacc[kb][r] = e;
         lsum += e;
       }
     l_run = l_run * alpha + lsum;
+    if (__any(alpha != 1.0f)) {  // some row's running max moved (alpha = 1 leaves O as it is)
 #pragma unroll
-    for (int db = 0; db < kDBlocks; ++db)
+      for (int db = 0; db < kDBlocks; ++db)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+    }
 
     // O^T += V^T P^T.  MFMA u of key block kb covers keys kb*32 + 16u + {4 half + 0..3,
     // 8 + 4 half + 0..3}, which are exactly accumulator registers 8u .. 8u+7 of sacc[kb].
