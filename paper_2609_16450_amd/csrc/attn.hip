@@ -97,7 +97,27 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
   // on the spot); keys past the end are replaced by zeros when stored to LDS.
   u32x4 kreg[kKPer];
   u32x4 vreg[2][kVd / 8];
+  const int key_stride = p.hkv * D;  // elements between consecutive keys of one K/V head
   auto gload = [&](int kv0) {
+    if (kv0 + kKeys <= plen) {
+      // the whole stage lies in the prefix: one base pointer per tensor, no per-key segment choice
+      const size_t base = (static_cast<size_t>(pbeg + kv0) * p.hkv + g) * D;
+      const uint16_t* kb = p.k_pre + base;
+      const uint16_t* vb = p.v_pre + base;
+#pragma unroll
+      for (int i = 0; i < kKPer; ++i) {
+        const int c = tid + i * kThreads;
+        const int key = c / (D / 8), col = (c % (D / 8)) * 8;
+        kreg[i] = *reinterpret_cast<const u32x4*>(kb + key * key_stride + col);
+      }
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int c = 0; c < kVd / 8; ++c)
+          vreg[e][c] = *reinterpret_cast<const u32x4*>(vb + (2 * kp + e) * key_stride +
+                                                       dg * kVd + 8 * c);
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < kKPer; ++i) {
       const int c = tid + i * kThreads;
