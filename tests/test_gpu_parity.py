@@ -338,3 +338,21 @@ def test_decode_step_matches_separate_entry_points(name, spec):
         if x.dtype == torch.bfloat16:
             x, y = x.view(torch.int16), y.view(torch.int16)
         assert torch.equal(x, y), field
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_decode_step_all_blocks_empty(dt):
+    # T = 0: no attention rows and no LM-head rows; the epilogue still settles every block
+    # (nothing to commit, nothing masked left).
+    say(f"decode_step with every block empty ({dt})")
+    case = make_step(custom_config("empty", seed=41, batch=3, hq=4, hkv=2, head_dim=64, hidden=128,
+                                   vocab=1000, block_len=("fixed", 0),
+                                   prefix_len=("uniform", 0, 40), dtype=dt))
+    assert case.T == 0
+    ds = DeviceStep(case)
+    ds.n_commit.fill_(-7)
+    ds.resolved.fill_(9)
+    eb_decode_step(ds.buffers)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ds.n_commit.cpu().numpy(), [0, 0, 0])
+    np.testing.assert_array_equal(ds.resolved.cpu().numpy(), [1, 1, 1])
