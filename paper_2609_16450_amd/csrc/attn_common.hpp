@@ -29,7 +29,8 @@ struct AttnParams {
   const uint16_t* k_suf;
   const uint16_t* v_suf;
   // key split: keys of a sequence are cut into ranges of kps keys, one workgroup per range;
-  // with nsplit > 1 the workgroups write unnormalised partials that attn_merge_kernel combines
+  // with nsplit > 1 the workgroups write unnormalised partials that attn_merge_kernel (or the
+  // fused step epilogue) combines
   int nsplit, kps;
   float* o_part;  // [T * hq * nsplit, D]
   float* m_part;  // [T * hq * nsplit]  running max (log2 units)
