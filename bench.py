@@ -32,7 +32,7 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
 MFMA_F32_PEAK_TFLOPS = 157.3    # fp32 vector peak (the fp32 path uses plain FMA)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lmhead_traffic.json")
 LMHEAD_SOURCES = [os.path.join(ROOT, "paper_2609_16450_amd", "csrc", f)
-                  for f in ("lmhead.hip", "eb_common.hpp")]
+                  for f in ("lmhead.hip", "eb_common.hpp", "attn_small.hpp", "attn_common.hpp")]
 
 
 def log(msg: str) -> None:

@@ -259,8 +259,13 @@ eb_status eb_lbs_select(int32_t n_seq, int32_t window, const uint8_t* masked,
  * with no host synchronisation.  Every output equals, bit for bit, what those three calls
  * produce; the step merely launches fewer kernels: the attention's key-split merge, the
  * merge of the LM-head partials and the unmask run as one epilogue launch (unless a block's
- * rows times the LM head's vocabulary slices exceed 65536, when they run separately).  The
- * workspace holds the attention's key-split partials followed by the LM-head partials.
+ * rows times the LM head's vocabulary slices exceed 65536, when they run separately), and in
+ * small bf16 steps (at most 64 block rows, at most 256 query rows per sequence and K/V head,
+ * head_dim 64 or 128, an LM head streamed by 16-wave workgroups) the attention's workgroups are
+ * queued behind the LM head's in the same launch, which starts them as the LM head's
+ * workgroups finish.  The attention does not depend on the LM head or the reverse, so this
+ * changes no result.  The workspace holds the attention's key-split partials followed by the
+ * LM-head partials.
  * Field meanings, layouts and requirements are those of the three calls above; the LM-head
  * rows are the block rows (n_rows = ragged.total_block).
  *
@@ -270,8 +275,10 @@ eb_status eb_lbs_select(int32_t n_seq, int32_t window, const uint8_t* masked,
  * ------------------------------------------------------------------------------------- */
 typedef struct {
   eb_event_t attn_begin, attn_end;     /* around the attention kernel (its split merge, if
-                                          any, runs in the epilogue) */
-  eb_event_t lmhead_begin, lmhead_end; /* around the fused LM-head kernel (without its merge) */
+                                          any, runs in the epilogue); recorded back to back
+                                          when the attention shares the LM-head launch */
+  eb_event_t lmhead_begin, lmhead_end; /* around the fused LM-head kernel (without its merge),
+                                          including the attention when it shares the launch */
   eb_event_t select_begin, select_end; /* around the epilogue: split merges and unmask */
 } eb_step_trace;
 

@@ -9,6 +9,7 @@
 // (an MFMA column) and reduces its softmax statistics in registers; the probabilities then
 // feed P V directly as the B operand of O^T = V^T P^T, with V staged transposed in LDS.
 #include "attn_common.hpp"
+#include "attn_small.hpp"
 #include "eb_common.hpp"
 #include "eb_internal.hpp"
 
@@ -19,13 +20,6 @@ constexpr int kThreads = 256;   // 4 waves
 constexpr int kRowsPerWg = kAttnRowsPerWg;
 constexpr int kKeys = kAttnKeys;
 
-
-// Two floats to two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32; lo in bits 0-15.
-__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
-  typedef float f32x2 __attribute__((ext_vector_type(2)));
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
-}
 
 // Two workgroups per compute unit (<= 256 VGPRs per lane, no spills at D = 128), so one
 // wave's softmax arithmetic overlaps another wave's MFMAs on the same SIMD (batch 64 at
@@ -270,6 +264,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
     }
 }
 
+// Small steps: the 16-query-row role of attn_small.hpp, one workgroup per unit.
+template <int D>
+__global__ __launch_bounds__(kSmallThreads) void attn_small_kernel(AttnParams p) {
+  attn_small_role<D>(p, static_cast<int>(blockIdx.x));
+}
+
 // Combine the key-split partials of each (block row, query head), one wavefront per pair.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p, int total_block, int batch) {
@@ -373,13 +373,21 @@ hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, 
   const SplitPlan sp = allow_split ? split_plan(a.batch, a.max_block, max_keys, a.hq, a.hkv)
                                    : SplitPlan{1, (max_keys + kKeys - 1) / kKeys * kKeys};
   const AttnParams p = attn_params(a, sp, ws);
-  const long rows = static_cast<long>(a.max_block) * group;
-  dim3 grid(static_cast<unsigned>((rows + kRowsPerWg - 1) / kRowsPerWg), a.hkv,
-            static_cast<unsigned>(a.batch) * sp.nsplit);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kThreads), 0, s, p);
-  else
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kThreads), 0, s, p);
+  if (allow_split && attn_small_ok(bf16, a)) {
+    const dim3 grid(static_cast<unsigned>(attn_small_units(a, sp)));
+    if (a.head_dim == 128)
+      hipLaunchKernelGGL(attn_small_kernel<128>, grid, dim3(kSmallThreads), 0, s, p);
+    else
+      hipLaunchKernelGGL(attn_small_kernel<64>, grid, dim3(kSmallThreads), 0, s, p);
+  } else {
+    const long rows = static_cast<long>(a.max_block) * group;
+    dim3 grid(static_cast<unsigned>((rows + kRowsPerWg - 1) / kRowsPerWg), a.hkv,
+              static_cast<unsigned>(a.batch) * sp.nsplit);
+    if (a.head_dim == 128)
+      hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kThreads), 0, s, p);
+    else
+      hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kThreads), 0, s, p);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || sp.nsplit == 1 || defer_merge) return e;
   const long pairs = static_cast<long>(a.total_block) * a.hq;

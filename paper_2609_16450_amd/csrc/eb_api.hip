@@ -344,13 +344,19 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
   const int n_slices = T > 0 ? eb::lmhead_num_slices(bf16, T, d->vocab) : 0;
   const bool fuse = eb::step_finish_fusable(r->max_block, n_slices);
 
+  // Small steps: the attention's workgroups ride in the LM-head launch, behind its slices (its
+  // split merge then happens in the epilogue, which is why this needs `fuse`).
+  const bool hosted = fuse && eb::lmhead_hosts_attn(bf16, T, d->vocab, a);
+
   hipError_t e = tr ? mark(tr->attn_begin) : hipSuccess;
-  if (e == hipSuccess) e = eb::block_attn(bf16, true, a, ws, stream, fuse);
+  if (e == hipSuccess && !hosted) e = eb::block_attn(bf16, true, a, ws, stream, fuse);
   if (e == hipSuccess && tr) e = mark(tr->attn_end);
   if (e != hipSuccess) return hip_status(e, "step attention launch");
 
   if (tr) e = mark(tr->lmhead_begin);
-  if (e == hipSuccess && T > 0)
+  if (e == hipSuccess && hosted)
+    e = eb::lmhead_partials_attn(T, d->hidden, d->vocab, d->h, d->w, lm_ws, a, ws, stream);
+  else if (e == hipSuccess && T > 0)
     e = eb::lmhead_partials(bf16, T, d->hidden, d->vocab, d->h, d->w, lm_ws, false, stream);
   if (e == hipSuccess && tr) e = mark(tr->lmhead_end);
   if (e != hipSuccess) return hip_status(e, "step LM-head launch");

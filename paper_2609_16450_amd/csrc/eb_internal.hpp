@@ -45,6 +45,14 @@ size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_blo
 hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, hipStream_t s,
                       bool defer_merge = false);
 
+// LM-head partials and the block attention of `a` in one launch: the attention's workgroups are
+// queued behind the LM head's vocabulary slices (key-split partials in attn_ws, merged by
+// step_finish).  Possible when lmhead_hosts_attn(...) holds; the attention then computes
+// exactly what block_attn computes for the same arguments.
+bool lmhead_hosts_attn(bool bf16, int n_rows, int vocab, const AttnArgs& a);
+hipError_t lmhead_partials_attn(int n_rows, int hidden, int vocab, const void* h, const void* w,
+                                void* ws, const AttnArgs& a, void* attn_ws, hipStream_t s);
+
 // ---- unmask ---------------------------------------------------------------------------
 hipError_t unmask_select(int batch, int max_block, const int32_t* cu_block, const float* conf,
                          const int32_t* argmax, const float* tau, uint8_t* masked,

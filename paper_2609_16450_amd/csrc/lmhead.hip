@@ -8,6 +8,7 @@
 // Orientation: the MFMA "row" dimension is the vocabulary and the "column" dimension is the
 // block position, so every lane owns one position and reduces the logits it holds in
 // registers before a single cross-half exchange.
+#include "attn_small.hpp"
 #include "eb_common.hpp"
 #include "eb_internal.hpp"
 
@@ -31,14 +32,10 @@ namespace {
 #endif
 constexpr int kStreamGroups = EB_STREAM_GROUPS;  // workgroups (256: one per compute unit)
 
-// The streaming kernel uses 16x16x32 MFMA tiles.  A lane of the A operand holds 8 consecutive
-// k-values of row l % 16 and the four lanes of a row cover 64 contiguous bytes, so each load
-// instruction reads 16 rows x 64 B of W (a 32x32x16 layout reads half that run per row and
-// measured 4.65 TB/s at best against 5.4).  Lane l of the f32x4 accumulator holds
-// C[4 (l / 16) + r][l % 16].
-__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
+// The streaming kernel uses 16x16x32 MFMA tiles (mfma16).  A lane of the A operand holds 8
+// consecutive k-values of row l % 16 and the four lanes of a row cover 64 contiguous bytes, so
+// each load instruction reads 16 rows x 64 B of W (a 32x32x16 layout reads half that run per row
+// and measured 4.65 TB/s at best against 5.4).
 
 // Second-largest logit (with multiplicity) of the union of two sets whose largest values are
 // m_a, m_b and second-largest m2_a, m2_b.  Exact and order-free, so every merge order gives
@@ -54,11 +51,20 @@ __device__ __forceinline__ float top2_shfl_merge(float m, float m2, int mask) {
 
 // kTop2: also track the second-largest logit of each (row, slice) into part2.
 // kWaves waves per workgroup, TM 16-row tiles per wave, NT 16-position tiles.
-template <int kWaves, int TM, int NT, int kDepth, bool kTop2>
+// kAttnD != 0: workgroups n_slices and up run the small block attention (head dimension kAttnD)
+// on unit blockIdx.x - n_slices of ap; the dispatcher starts them as the slices finish.
+template <int kWaves, int TM, int NT, int kDepth, bool kTop2, int kAttnD>
 __global__ __launch_bounds__(kWaves * 64) void lmhead_stream16_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
     int vocab, int rows_per_wg, Partial* __restrict__ part, float* __restrict__ part2,
-    int n_slices) {
+    int n_slices, AttnParams ap) {
+  static_assert(kAttnD == 0 || kWaves * 64 == kSmallThreads, "attention role shape");
+  if constexpr (kAttnD != 0) {
+    if (static_cast<int>(blockIdx.x) >= n_slices) {  // whole workgroup
+      attn_small_role<kAttnD>(ap, static_cast<int>(blockIdx.x) - n_slices);
+      return;
+    }
+  }
   constexpr int KC = 1024 / NT;        // h columns per LDS chunk
   constexpr int kPitch = KC + 8;       // LDS row pitch (bf16)
   constexpr int kSpc = KC / 32;        // k-steps per chunk
@@ -261,10 +267,16 @@ bool use_stream(int n_rows, int vocab) {
   return pl.tm <= kStreamMaxTm8;
 }
 
-template <int kWaves, int TM, int NT, bool kTop2>
+// Block attention queued behind the slices of a streaming launch (attn_d 0: none).
+struct HostedAttn {
+  AttnParams p;
+  int units, attn_d;
+};
+
+template <int kWaves, int TM, int NT, bool kTop2, int kAttnD = 0>
 hipError_t launch_stream_tm(int n_rows, int hidden, int vocab, const StreamPlan& pl,
                             const void* h, const void* w, Partial* part, float* part2,
-                            hipStream_t s) {
+                            hipStream_t s, const HostedAttn& ha) {
   // 16 waves: up to 16 W registers in flight per lane (16 bytes each; 8 with four position
   // tiles), at most kStreamDepth k-steps.  8 waves: two k-steps (more measured no faster).
   constexpr int kBudget = kWaves == 8 ? 2 * TM : (NT >= 4 ? 8 : 16);
@@ -272,41 +284,60 @@ hipError_t launch_stream_tm(int n_rows, int hidden, int vocab, const StreamPlan&
   constexpr int D = (kWaves == 16 && D0 > kStreamDepth) ? kStreamDepth : D0;
   // a power of two that divides the per-chunk step count
   constexpr int Dp = D >= 8 ? 8 : (D >= 4 ? 4 : (D >= 2 ? 2 : 1));
-  hipLaunchKernelGGL((lmhead_stream16_kernel<kWaves, TM, NT, Dp, kTop2>), dim3(pl.groups),
-                     dim3(kWaves * 64), 0, s, static_cast<const uint16_t*>(h),
-                     static_cast<const uint16_t*>(w), n_rows, hidden, vocab, pl.rows_per_wg, part,
-                     part2, pl.groups);
+  const int extra = kAttnD != 0 ? ha.units : 0;
+  hipLaunchKernelGGL((lmhead_stream16_kernel<kWaves, TM, NT, Dp, kTop2, kAttnD>),
+                     dim3(pl.groups + extra), dim3(kWaves * 64), 0, s,
+                     static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w), n_rows,
+                     hidden, vocab, pl.rows_per_wg, part, part2, pl.groups, ha.p);
   return hipGetLastError();
+}
+
+// 16 waves, TM row tiles: the variant for the hosted attention's head dimension.
+template <int TM, int NT, bool kTop2>
+hipError_t launch_stream16(int n_rows, int hidden, int vocab, const StreamPlan& pl,
+                           const void* h, const void* w, Partial* part, float* part2,
+                           hipStream_t s, const HostedAttn& ha) {
+  if constexpr (!kTop2) {
+    if (ha.attn_d == 128)
+      return launch_stream_tm<16, TM, NT, false, 128>(n_rows, hidden, vocab, pl, h, w, part,
+                                                      part2, s, ha);
+    if (ha.attn_d == 64)
+      return launch_stream_tm<16, TM, NT, false, 64>(n_rows, hidden, vocab, pl, h, w, part,
+                                                     part2, s, ha);
+  }
+  if (ha.attn_d != 0) return hipErrorInvalidValue;  // excluded by lmhead_hosts_attn
+  return launch_stream_tm<16, TM, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s,
+                                             ha);
 }
 
 // NT: 16-position tiles covering n_rows.
 template <int NT, bool kTop2>
 hipError_t launch_stream(int n_rows, int hidden, int vocab, const void* h, const void* w,
-                         Partial* part, float* part2, hipStream_t s) {
+                         Partial* part, float* part2, hipStream_t s, const HostedAttn& ha) {
   const StreamPlan pl = stream_plan(vocab);
   if (pl.waves == 16) {
     switch (pl.tm) {
       case 1:
-        return launch_stream_tm<16, 1, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2,
-                                                    s);
+        return launch_stream16<1, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s, ha);
       case 2:
-        return launch_stream_tm<16, 2, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2,
-                                                    s);
+        return launch_stream16<2, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s, ha);
       case 3:
-        return launch_stream_tm<16, 3, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2,
-                                                    s);
+        return launch_stream16<3, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s, ha);
       default: return hipErrorInvalidValue;  // excluded by stream_plan
     }
   }
+  if (ha.attn_d != 0) return hipErrorInvalidValue;  // excluded by lmhead_hosts_attn
   // More than 48 tiles of rows per workgroup: the 8-wave shape has 7 or 8 tiles per wave.
   switch (pl.tm) {
     case 7:
       if constexpr (NT < 4)
-        return launch_stream_tm<8, 7, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+        return launch_stream_tm<8, 7, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s,
+                                                 ha);
       return hipErrorInvalidValue;
     case 8:
       if constexpr (NT < 4)
-        return launch_stream_tm<8, 8, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s);
+        return launch_stream_tm<8, 8, NT, kTop2>(n_rows, hidden, vocab, pl, h, w, part, part2, s,
+                                                 ha);
       return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;  // excluded by use_stream
   }
@@ -314,10 +345,14 @@ hipError_t launch_stream(int n_rows, int hidden, int vocab, const void* h, const
 
 template <bool kTop2>
 hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, const void* w,
-                              Partial* part, float* part2, hipStream_t s) {
-  if (n_rows <= 16) return launch_stream<1, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s);
-  if (n_rows <= 32) return launch_stream<2, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s);
-  if (n_rows <= 64) return launch_stream<4, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s);
+                              Partial* part, float* part2, hipStream_t s,
+                              const HostedAttn& ha = HostedAttn{}) {
+  if (n_rows <= 16)
+    return launch_stream<1, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s, ha);
+  if (n_rows <= 32)
+    return launch_stream<2, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s, ha);
+  if (n_rows <= 64)
+    return launch_stream<4, kTop2>(n_rows, hidden, vocab, h, w, part, part2, s, ha);
   return hipErrorInvalidValue;  // excluded by use_stream
 }
 
@@ -917,6 +952,19 @@ hipError_t lmhead_partials(bool bf16, int n_rows, int hidden, int vocab, const v
                 : launch_stream_rows<false>(n_rows, hidden, vocab, h, w, part, part2, s);
   return top2 ? launch_tile<true>(n_rows, hidden, vocab, h, w, part, part2, s)
               : launch_tile<false>(n_rows, hidden, vocab, h, w, part, part2, s);
+}
+
+bool lmhead_hosts_attn(bool bf16, int n_rows, int vocab, const AttnArgs& a) {
+  return bf16 && n_rows > 0 && use_stream(n_rows, vocab) && stream_plan(vocab).waves == 16 &&
+         attn_small_ok(bf16, a);
+}
+
+hipError_t lmhead_partials_attn(int n_rows, int hidden, int vocab, const void* h, const void* w,
+                                void* ws, const AttnArgs& a, void* attn_ws, hipStream_t s) {
+  const SplitPlan sp = split_plan(a.batch, a.max_block, attn_max_keys(a), a.hq, a.hkv);
+  const HostedAttn ha{attn_params(a, sp, attn_ws), attn_small_units(a, sp), a.head_dim};
+  return launch_stream_rows<false>(n_rows, hidden, vocab, h, w, static_cast<Partial*>(ws),
+                                   nullptr, s, ha);
 }
 
 hipError_t lmhead_combine(bool bf16, int n_rows, int vocab, const void* ws, float* conf,

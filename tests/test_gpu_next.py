@@ -260,6 +260,7 @@ DUAL_CASES = [
     (4, 8, 2, 128, ("uniform", 0, 40), ("uniform", 0, 200), [0, 65, 1, 130], "bf16"),
     (3, 28, 4, 128, ("uniform", 10, 60), ("fixed", 300), [64, 0, 200], "bf16"),
     (5, 4, 1, 64, ("choice", (1, 63, 64, 65, 129)), ("choice", (0, 1, 64)), [0, 1, 63, 64, 300], "bf16"),
+    (2, 8, 2, 64, ("fixed", 16), ("uniform", 0, 90), [70, 0], "bf16"),  # small-step kernel
 ]
 
 

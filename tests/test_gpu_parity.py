@@ -126,6 +126,14 @@ ATTN_CASES = [
     (3, 6, 6, 64, ("uniform", 1, 70), ("uniform", 60, 130), "bf16"),
     (2, 28, 4, 128, ("uniform", 10, 60), ("fixed", 300), "bf16"),
     (5, 4, 1, 128, ("choice", (0, 1, 63, 64, 65, 129)), ("choice", (0, 1, 63, 64, 65)), "bf16"),
+    # small steps (<= 64 block rows, <= 256 query rows per sequence and K/V head) take the
+    # 16-row kernel that also runs inside the LM-head launch of a step
+    (1, 32, 32, 128, ("fixed", 32), ("fixed", 512), "bf16"),    # batch-1 LLaDA shape, 9 ranges
+    (1, 32, 8, 128, ("fixed", 64), ("fixed", 200), "bf16"),     # 256 query rows: all 16 waves
+    (4, 8, 2, 64, ("uniform", 0, 16), ("uniform", 0, 150), "bf16"),  # D = 64, empty blocks
+    (3, 4, 4, 128, ("choice", (1, 5, 17)), ("choice", (0, 1, 63)), "bf16"),  # one range: no split
+    (2, 28, 4, 128, ("fixed", 32), ("fixed", 700), "bf16"),     # G = 7: 224 rows, 14 waves
+    (8, 16, 2, 64, ("fixed", 8), ("uniform", 300, 1100), "bf16"),  # G = 8, many key ranges
 ]
 
 
@@ -314,6 +322,17 @@ FUSE_CASES = [
     # too many partials for one workgroup per block: separate kernels
     ("long_block", dict(seed=32, batch=1, hq=2, hkv=2, head_dim=64, hidden=64, vocab=60000,
                         block_len=("fixed", 300), prefix_len=("fixed", 64))),
+    # small steps: the attention runs inside the LM-head launch (key split merged in the
+    # epilogue, or no split at all)
+    ("hosted_gqa_d64", dict(seed=34, batch=4, hq=8, hkv=2, head_dim=64, hidden=256, vocab=7000,
+                            block_len=("uniform", 0, 16), prefix_len=("uniform", 0, 150))),
+    ("hosted_no_split", dict(seed=35, batch=2, hq=4, hkv=4, head_dim=128, hidden=128,
+                             vocab=3000, block_len=("fixed", 20), prefix_len=("fixed", 10))),
+    ("hosted_256_rows", dict(seed=36, batch=1, hq=16, hkv=4, head_dim=128, hidden=512,
+                             vocab=20000, block_len=("fixed", 64), prefix_len=("fixed", 333))),
+    # small attention, but an 8-wave LM-head launch: the attention runs on its own
+    ("small_attn_8wave_lm", dict(seed=37, batch=1, hq=4, hkv=4, head_dim=128, hidden=64,
+                                 vocab=262144, block_len=("fixed", 16), prefix_len=("fixed", 100))),
     # fp32 path
     ("f32", dict(seed=33, batch=3, hq=4, hkv=2, head_dim=64, hidden=128, vocab=999,
                  block_len=("uniform", 1, 20), prefix_len=("uniform", 0, 50), dtype="f32")),
