@@ -264,10 +264,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
     }
 }
 
-// Small steps: the 16-query-row role of attn_small.hpp, one workgroup per unit.
+// Small steps on their own: the 16-query-row role of attn_small.hpp with kSmallAloneThreads
+// threads, one workgroup per (unit, group of row tiles).
+#ifndef EB_SMALL_ALONE_THREADS
+#define EB_SMALL_ALONE_THREADS 256
+#endif
+constexpr int kSmallAloneThreads = EB_SMALL_ALONE_THREADS;
 template <int D>
-__global__ __launch_bounds__(kSmallThreads) void attn_small_kernel(AttnParams p) {
-  attn_small_role<D>(p, static_cast<int>(blockIdx.x));
+__global__ __launch_bounds__(kSmallAloneThreads) void attn_small_kernel(AttnParams p) {
+  attn_small_role<D, kSmallAloneThreads>(p, static_cast<int>(blockIdx.x),
+                                          static_cast<int>(blockIdx.y));
 }
 
 // Combine the key-split partials of each (block row, query head), one wavefront per pair.
@@ -374,11 +380,14 @@ hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, 
                                    : SplitPlan{1, (max_keys + kKeys - 1) / kKeys * kKeys};
   const AttnParams p = attn_params(a, sp, ws);
   if (allow_split && attn_small_ok(bf16, a)) {
-    const dim3 grid(static_cast<unsigned>(attn_small_units(a, sp)));
+    const long tiles = (static_cast<long>(a.max_block) * group + kSmallTile - 1) / kSmallTile;
+    const int waves = kSmallAloneThreads / 64;
+    const dim3 grid(static_cast<unsigned>(attn_small_units(a, sp)),
+                    static_cast<unsigned>((tiles + waves - 1) / waves));
     if (a.head_dim == 128)
-      hipLaunchKernelGGL(attn_small_kernel<128>, grid, dim3(kSmallThreads), 0, s, p);
+      hipLaunchKernelGGL(attn_small_kernel<128>, grid, dim3(kSmallAloneThreads), 0, s, p);
     else
-      hipLaunchKernelGGL(attn_small_kernel<64>, grid, dim3(kSmallThreads), 0, s, p);
+      hipLaunchKernelGGL(attn_small_kernel<64>, grid, dim3(kSmallAloneThreads), 0, s, p);
   } else {
     const long rows = static_cast<long>(a.max_block) * group;
     dim3 grid(static_cast<unsigned>((rows + kRowsPerWg - 1) / kRowsPerWg), a.hkv,

@@ -42,10 +42,12 @@ inline int attn_small_units(const AttnArgs& a, const SplitPlan& sp) {
   return a.batch * a.hkv * sp.nsplit;
 }
 
-// Attention role of unit `unit` (= (b hkv + g) nsplit + split); every thread of the workgroup
-// calls it, and every thread returns from it.
-template <int D>
-__device__ __forceinline__ void attn_small_role(const AttnParams& p, int unit) {
+// Attention role of unit `unit` (= (b hkv + g) nsplit + split) for the query-row tiles
+// tile_group * kThreads/64 .. +kThreads/64 - 1 of its (sequence, K/V head), one per wave; every
+// thread of the workgroup calls it, and every thread returns from it.  A row's arithmetic does
+// not depend on kThreads, so every workgroup size gives the same bits.
+template <int D, int kThreads>
+__device__ __forceinline__ void attn_small_role(const AttnParams& p, int unit, int tile_group) {
   constexpr int kKeys = kAttnKeys;    // keys per stage
   constexpr int kKPitch = D + 8;      // K row pitch (bf16)
   constexpr int kVPitch = D + 16;     // V row pitch (bf16): 16 rows x 32 B of a transposed read
@@ -53,7 +55,8 @@ __device__ __forceinline__ void attn_small_role(const AttnParams& p, int unit) {
   constexpr int kDSteps = D / 32;     // MFMA k-steps of S^T over the head dimension
   constexpr int kDTiles = D / 16;     // 16-row tiles of O^T
   constexpr int kChunks = kKeys * D / 8;  // 16-byte pieces of one K (or V) stage
-  static_assert(kChunks <= kSmallThreads, "one piece per thread");
+  constexpr int kPer = kChunks >= kThreads ? kChunks / kThreads : 1;  // pieces per thread
+  static_assert(kChunks % kThreads == 0 || kThreads % kChunks == 0, "pieces split evenly");
   __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeys * kKPitch];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[kKeys * kVPitch];
 
@@ -70,13 +73,14 @@ __device__ __forceinline__ void attn_small_role(const AttnParams& p, int unit) {
   const int n_keys = plen + len + slen;
   const int n_rows = len * G;
   const int kbeg = sp * p.kps;
-  if (n_rows == 0 || kbeg >= n_keys) return;  // whole workgroup: nothing in this range
+  const int row0 = tile_group * (kThreads / 64) * kSmallTile;
+  if (row0 >= n_rows || kbeg >= n_keys) return;  // whole workgroup: nothing to do here
   const int kend = min(n_keys, kbeg + p.kps);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = lane >> 4, l16 = lane & 15;
-  const bool active = wave * kSmallTile < n_rows;  // wave-uniform: the wave owns query rows
-  const int myrow = wave * kSmallTile + l16;
+  const bool active = row0 + wave * kSmallTile < n_rows;  // wave-uniform: the wave owns rows
+  const int myrow = row0 + wave * kSmallTile + l16;
   const bool row_ok = myrow < n_rows;
   const int rr = row_ok ? myrow : n_rows - 1;
   const int pos = rr / G, hh = rr % G;
@@ -100,21 +104,30 @@ __device__ __forceinline__ void attn_small_role(const AttnParams& p, int unit) {
     if (j < plen + len) return blk + (static_cast<size_t>(bbeg + j - plen) * p.hkv + g) * D;
     return suf + (static_cast<size_t>(sbeg + j - plen - len) * p.hkv + g) * D;
   };
-  // Thread tid < kChunks moves piece tid of K and of V: key tid / (D/8), columns 8 (tid % (D/8)).
-  // Keys past the end are loaded from a clamped, valid row; their scores are set to -inf.
+  // Thread tid moves pieces tid + i kThreads (i < kPer) of K and of V: piece c is key c / (D/8),
+  // columns 8 (c % (D/8)).  Keys past the end are loaded from a clamped, valid row; their scores
+  // are set to -inf.
   const bool loader = tid < kChunks;  // wave-uniform (kChunks is a multiple of 64)
-  const int lkey = tid / (D / 8), lcol = (tid % (D / 8)) * 8;
-  u32x4 kreg{}, vreg{};
+  u32x4 kreg[kPer], vreg[kPer];
   auto gload = [&](int kv0) {
     if (!loader) return;
-    const int j = min(kv0 + lkey, kend - 1);
-    kreg = *reinterpret_cast<const u32x4*>(key_src(j, p.k_pre, p.k_blk, p.k_suf) + lcol);
-    vreg = *reinterpret_cast<const u32x4*>(key_src(j, p.v_pre, p.v_blk, p.v_suf) + lcol);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = tid + i * kThreads;
+      const int j = min(kv0 + c / (D / 8), kend - 1), col = (c % (D / 8)) * 8;
+      kreg[i] = *reinterpret_cast<const u32x4*>(key_src(j, p.k_pre, p.k_blk, p.k_suf) + col);
+      vreg[i] = *reinterpret_cast<const u32x4*>(key_src(j, p.v_pre, p.v_blk, p.v_suf) + col);
+    }
   };
   auto sstore = [&]() {
     if (!loader) return;
-    *reinterpret_cast<u32x4*>(Ks + lkey * kKPitch + lcol) = kreg;
-    *reinterpret_cast<u32x4*>(Vs + lkey * kVPitch + lcol) = vreg;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = tid + i * kThreads;
+      const int key = c / (D / 8), col = (c % (D / 8)) * 8;
+      *reinterpret_cast<u32x4*>(Ks + key * kKPitch + col) = kreg[i];
+      *reinterpret_cast<u32x4*>(Vs + key * kVPitch + col) = vreg[i];
+    }
   };
   // V^T fragment for keys kbase + 4 grp + 0..3 at d = d0 + l16: lanes 4j .. 4j+3 of a 16-lane
   // group address row kbase + 4 grp + j, columns d0 + 4 (l16 % 4) .. +3; the transposed read

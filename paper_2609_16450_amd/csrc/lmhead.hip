@@ -61,7 +61,7 @@ __global__ __launch_bounds__(kWaves * 64) void lmhead_stream16_kernel(
   static_assert(kAttnD == 0 || kWaves * 64 == kSmallThreads, "attention role shape");
   if constexpr (kAttnD != 0) {
     if (static_cast<int>(blockIdx.x) >= n_slices) {  // whole workgroup
-      attn_small_role<kAttnD>(ap, static_cast<int>(blockIdx.x) - n_slices);
+      attn_small_role<kAttnD, kSmallThreads>(ap, static_cast<int>(blockIdx.x) - n_slices, 0);
       return;
     }
   }
