@@ -36,6 +36,15 @@ __global__ __launch_bounds__(kFinishThreads) void step_finish_kernel(
   }
   const int b = blockIdx.x - n_merge;
   const int beg = ap.cu_block[b], end = ap.cu_block[b + 1];
+  // A block of at most 64 rows also leaves its rows' conf and argmax in LDS, and wave 0 then runs
+  // the block step alone (one barrier, no reduction across waves; its lanes read their rows' mask
+  // flags up front).  Larger blocks run the workgroup-wide step.
+  const bool small = end - beg <= 64;
+  __shared__ float s_conf[64];
+  __shared__ int32_t s_arg[64];
+  const int own_row = beg + lane;
+  const bool own_ok = small && wave == 0 && own_row < end;
+  const uint8_t m_own = own_ok ? masked[own_row] : uint8_t{0};
   // Wave w reduces rows beg + w, beg + w + 16, ...; kRowBatch rows at a time with their loads in
   // flight together and their merges interleaved.  Each row is merged exactly as wave_merge does
   // it (lane-strided in index order, loads grouped by 4, an empty partial in place of a missing
@@ -65,10 +74,23 @@ __global__ __launch_bounds__(kFinishThreads) void step_finish_kernel(
     for (int i = 0; i < kRowBatch; ++i) {
       const Partial p = wave_finish(acc[i]);
       const int row = r0 + kWaves * i;
-      if (lane == 0 && row < end) write_row_stats(p, row, conf, entropy, argmax, max_logit);
+      if (lane == 0 && row < end) {
+        write_row_stats(p, row, conf, entropy, argmax, max_logit);
+        if (small) {
+          s_conf[row - beg] = 1.0f / p.s;  // the value write_row_stats stores
+          s_arg[row - beg] = p.idx;
+        }
+      }
     }
   }
   __syncthreads();  // the block's conf / argmax rows are written before the block step reads them
+  if (small) {
+    if (wave == 0)
+      unmask_wave_threshold(b, own_row, own_ok, m_own, own_ok ? s_conf[lane] : 0.f,
+                            own_ok ? s_arg[lane] : 0, tau[b], masked, tokens, unmask, n_commit,
+                            resolved, lane);
+    return;
+  }
   unmask_block<kThreshold, kFinishThreads>(b, ap.cu_block, conf, argmax, tau,
                                            RuleArgs{nullptr, 0.f, 0}, masked, tokens, unmask,
                                            n_commit, resolved);

@@ -78,6 +78,42 @@ __device__ __forceinline__ void rank_rows(int beg, int end, const float* __restr
   }
 }
 
+// Threshold step of a block of at most 64 rows by one wavefront (the rule, tie-break and commit
+// of unmask_block<kThreshold>): lane l holds row `row` (valid when `mine`), its mask flag m, its
+// conf c and its top-1 token x; tb is the block's tau.
+__device__ __forceinline__ void unmask_wave_threshold(int b, int row, bool mine, uint8_t m,
+                                                      float c, int32_t x, float tb,
+                                                      uint8_t* __restrict__ masked,
+                                                      int32_t* __restrict__ tokens,
+                                                      uint8_t* __restrict__ unmask,
+                                                      int32_t* __restrict__ n_commit,
+                                                      uint8_t* __restrict__ resolved, int lane) {
+  const bool mk = mine && m;
+  int n_masked = mk ? 1 : 0;
+  int n_pass = (mk && c >= tb) ? 1 : 0;
+  Best best = mk ? Best{c, row} : Best{-INFINITY, kNoIndex};
+  for (int mask = 32; mask >= 1; mask >>= 1) {
+    n_masked += __shfl_xor(n_masked, mask);
+    n_pass += __shfl_xor(n_pass, mask);
+    Best o{__shfl_xor(best.c, mask), __shfl_xor(best.i, mask)};
+    best = best_of(best, o);
+  }
+  const bool use_rule = n_pass > 0;
+  if (mine) {
+    const bool take = mk && (use_rule ? c >= tb : row == best.i);
+    unmask[row] = take ? 1 : 0;
+    if (take) {
+      tokens[row] = x;
+      masked[row] = 0;
+    }
+  }
+  if (lane == 0) {
+    const int commits = use_rule ? n_pass : (n_masked > 0 ? 1 : 0);
+    n_commit[b] = commits;
+    resolved[b] = (n_masked - commits == 0) ? 1 : 0;
+  }
+}
+
 // Step of block b by one workgroup of kThreads threads under rule R (the top-m rank count runs
 // on kUnmaskThreads threads).
 template <Rule R, int kThreads = kUnmaskThreads>
