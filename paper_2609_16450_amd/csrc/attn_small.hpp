@@ -1,17 +1,19 @@
-// Block attention for small steps (at most 64 block rows in all), written as the role of one
-// 1024-thread workgroup with at most 128 VGPRs per lane.  The same role runs as a kernel of its
-// own (attn_small_kernel) and as extra workgroups of the streaming LM-head launch, queued behind
-// its vocabulary slices: the dispatcher starts them on the compute units that the slices free
-// at the end, so the attention fills the LM head's tail instead of taking a launch of its own.
+// Block attention for small steps (at most 64 block rows in all), written as the role of a
+// workgroup of up to 1024 threads that stays within 128 VGPRs per lane at that size.  The role
+// runs as a kernel of its own (attn_small_kernel, 256-thread workgroups) and, with 1024 threads,
+// as extra workgroups of the streaming LM-head launch, queued behind its vocabulary slices: the
+// dispatcher starts them on the compute units that the slices free at the end, so the attention
+// fills the LM head's tail instead of taking a launch of its own.
 //
-// One workgroup per (sequence b, K/V head g, key range): the query rows of (b, g) are the
-// (position, head-in-group) pairs, 16 per wave (at most 16 x 16 = 256 rows, so one workgroup
-// holds them all); all 16 waves stage each 64-key stage of K and V in LDS, the waves that own
-// query rows compute.  Scores are formed transposed, S^T = K Q^T, with 16x16x32 MFMAs, so lane l
-// owns query l % 16 and holds keys 4 (l / 16) + r of each 16-key tile; exactly those keys are
-// the k-slots of the B operand of O^T = V^T P^T once the contraction index is permuted, and the
-// matching V^T operand comes from two transposed LDS reads (ds_read_b64_tr_b16) of row-major V.
-// Same key split, partial layout and online-softmax convention as the 128-row kernel.
+// One workgroup per (sequence b, K/V head g, key range) and group of 16-row query tiles: the
+// query rows of (b, g) are the (position, head-in-group) pairs, 16 per wave (at most 256 rows,
+// one 1024-thread workgroup for all of them); the workgroup stages each 64-key stage of K and V
+// in LDS, and the waves that own query rows compute.  Scores are formed transposed,
+// S^T = K Q^T, with 16x16x32 MFMAs, so lane l owns query l % 16 and holds keys 4 (l / 16) + r of
+// each 16-key tile; exactly those keys are the k-slots of the B operand of O^T = V^T P^T once
+// the contraction index is permuted, and the matching V^T operand comes from two transposed LDS
+// reads (ds_read_b64_tr_b16) of row-major V.  Same key split, partial layout and online-softmax
+// convention as the 128-row kernel.
 #pragma once
 
 #include "attn_common.hpp"
@@ -20,7 +22,7 @@
 namespace eb {
 namespace {
 
-constexpr int kSmallThreads = 1024;                 // 16 waves
+constexpr int kSmallThreads = 1024;                 // 16 waves (inside the LM-head launch)
 constexpr int kSmallTile = 16;                      // query rows per wave
 constexpr int kSmallMaxRows = 16 * kSmallTile;      // query rows of one (sequence, K/V head)
 constexpr int kSmallMaxTotal = 64;                  // block rows of the whole step
@@ -50,8 +52,9 @@ template <int D, int kThreads>
 __device__ __forceinline__ void attn_small_role(const AttnParams& p, int unit, int tile_group) {
   constexpr int kKeys = kAttnKeys;    // keys per stage
   constexpr int kKPitch = D + 8;      // K row pitch (bf16)
-  constexpr int kVPitch = D + 16;     // V row pitch (bf16): 16 rows x 32 B of a transposed read
-                                      // fall on distinct banks
+  constexpr int kVPitch = D + 16;     // V row pitch (bf16): rows 8 banks apart, so the 8 rows
+                                      // x 32 B that 32 lanes of a transposed read touch fall on
+                                      // distinct banks
   constexpr int kDSteps = D / 32;     // MFMA k-steps of S^T over the head dimension
   constexpr int kDTiles = D / 16;     // 16-row tiles of O^T
   constexpr int kChunks = kKeys * D / 8;  // 16-byte pieces of one K (or V) stage
