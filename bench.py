@@ -18,6 +18,7 @@ import json
 import math
 import os
 import platform
+import re
 import sys
 import time
 
@@ -40,10 +41,14 @@ def log(msg: str) -> None:
 
 
 def lmhead_source_hash() -> str:
+    """Hash of the code (comments and whitespace removed) of the LM-head launch's sources."""
     h = hashlib.sha256()
     for p in LMHEAD_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p, encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
