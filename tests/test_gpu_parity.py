@@ -375,3 +375,46 @@ def test_decode_step_all_blocks_empty(dt):
     torch.cuda.synchronize()
     np.testing.assert_array_equal(ds.n_commit.cpu().numpy(), [0, 0, 0])
     np.testing.assert_array_equal(ds.resolved.cpu().numpy(), [1, 1, 1])
+
+
+_STEP_FIELDS = ("attn_out", "conf", "entropy", "argmax", "max_logit", "tokens", "masked", "unmask",
+                "n_commit", "resolved")
+
+
+@pytest.mark.parametrize("name,spec", [
+    ("llada8b_b1", None),  # attention inside the LM-head launch, fused epilogue
+    ("ragged", dict(seed=31, batch=5, hq=8, hkv=2, head_dim=128, hidden=256, vocab=5000,
+                    block_len=("uniform", 0, 40), prefix_len=("uniform", 0, 300))),
+], ids=["llada8b_b1", "ragged"])
+def test_decode_step_hip_graph_replays(name, spec):
+    # The step allocates nothing and records no memset, so it can be captured in a HIP graph.
+    # Each replay, with eager steps and host synchronisations between replays, must equal an
+    # eager step on the same inputs bit for bit.
+    say(f"decode_step captured in a HIP graph: {name}")
+    case = make_step(name if spec is None else custom_config(name, **spec))
+    g_in, e_in = DeviceStep(case), DeviceStep(case)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        eb_decode_step(g_in.buffers)  # warm-up outside the capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    g_in.reset_state()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        eb_decode_step(g_in.buffers)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        g_in.reset_state()
+        e_in.reset_state()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        eb_decode_step(e_in.buffers)
+        torch.cuda.synchronize()
+        for field in _STEP_FIELDS:
+            x, y = getattr(g_in, field), getattr(e_in, field)
+            if x.dtype == torch.bfloat16:
+                x, y = x.view(torch.int16), y.view(torch.int16)
+            assert torch.equal(x, y), (rep, field)
