@@ -418,3 +418,42 @@ def test_decode_step_hip_graph_replays(name, spec):
             if x.dtype == torch.bfloat16:
                 x, y = x.view(torch.int16), y.view(torch.int16)
             assert torch.equal(x, y), (rep, field)
+
+
+def _random_step_spec(i):
+    # Seeded shapes around the dispatch boundaries of the step: total block rows near 64 (the
+    # small-step attention and the streaming LM head), query rows per K/V head near 256, both
+    # head dimensions, GQA groups 1-8, empty blocks, vocabularies for 16- and 8-wave streaming.
+    r = np.random.default_rng(9000 + i)
+    hq, hkv = [(4, 4), (8, 2), (16, 4), (28, 4), (32, 32), (12, 3), (32, 4)][r.integers(7)]
+    batch = int(r.integers(1, 5))
+    hi = int(r.choice([8, 16, 24, 40, 70]))
+    return dict(seed=700 + i, batch=batch, hq=hq, hkv=hkv, head_dim=int(r.choice([64, 128])),
+                hidden=int(r.choice([64, 128, 256])),
+                vocab=int(r.choice([2000, 9000, 33000, 200000, 250000])),
+                block_len=("uniform", 0, hi), prefix_len=("uniform", 0, int(r.integers(1, 700))))
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_decode_step_random_shapes(i):
+    spec = _random_step_spec(i)
+    say(f"decode_step random shape {i}: {spec}")
+    case = make_step(custom_config(f"random{i}", **spec))
+    a = DeviceStep(case)
+    eb_decode_step(a.buffers)
+    b = DeviceStep(case)
+    eb_block_attn(b.ragged, b.q, b.k_blk, b.v_blk, b.k_pre, b.v_pre, b.attn_out)
+    eb_lmhead_confidence(b.h, b.w, b.conf, b.entropy, b.argmax, b.max_logit)
+    eb_unmask_select(b.ragged, b.conf, b.argmax, b.tau, b.masked, b.tokens, b.unmask, b.n_commit,
+                     b.resolved)
+    torch.cuda.synchronize()
+    for field in _STEP_FIELDS:
+        x, y = getattr(a, field), getattr(b, field)
+        if x.dtype == torch.bfloat16:
+            x, y = x.view(torch.int16), y.view(torch.int16)
+        assert torch.equal(x, y), field
+    if case.T:
+        f = {k: as_f32(getattr(case, k), "bf16") for k in ("q", "k_blk", "v_blk", "k_pre", "v_pre")}
+        ref = oracle.block_attention(**f, cu_block=case.cu_block, cu_prefix=case.cu_prefix,
+                                     hq=spec["hq"], hkv=spec["hkv"])
+        np.testing.assert_allclose(attn_out_f32(a.attn_out), ref, **ATTN_TOL_BF16)
