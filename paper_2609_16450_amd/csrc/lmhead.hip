@@ -357,14 +357,14 @@ hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, 
 }
 
 // ---------------------------------------------------------------------------------------
-// Large-batch kernels: 256 (vocabulary) x BN (positions) tiles.
+// Large-batch kernel: 256 (vocabulary) x 256 (positions) tiles.
 //
 // Both operands are streamed HBM -> LDS by direct loads (global_load_lds_dwordx4: lane l of a
 // wave writes its 16 bytes to LDS base + 16 l) into a ring of RING stages of BK = 32 hidden
 // columns, RING - 1 stages in flight; no staging registers and no LDS store instructions.  LDS
 // rows are 64 bytes without padding; the 16-byte chunk c of row r is kept in slot
 // c ^ ((r / 4) % 4), which makes the 32-row MFMA operand reads free of bank conflicts.
-// Waves form a 2 x WN grid of 128 x (BN / WN) sub-tiles of 32x32x16 MFMA blocks.
+// Four waves form a 2 x 2 grid of 128 x 128 sub-tiles of 32x32x16 MFMA blocks.
 //
 // Launch order is XCD-aware: vocabulary tiles are grouped in bands of kBand, band b goes to XCD
 // b % 8 (workgroups are dealt to the 8 XCDs round-robin by id), and each XCD sweeps its band row
@@ -397,34 +397,6 @@ __device__ __forceinline__ void load_to_lds(const void* g, void* l) {
   // address-space casts (generic -> global / LDS) need C-style casts
   __builtin_amdgcn_global_load_lds((global_void_t*)(const_cast<void*>(g)), (lds_void_t*)(l), 16, 0,
                                    0);
-}
-
-// Wait until at most N vector-memory instructions of this wave are outstanding, then barrier.
-// The memory clobber keeps the compiler from moving LDS accesses across it.
-template <int N>
-__device__ __forceinline__ void wait_vm_and_barrier() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
-  asm volatile("s_barrier" ::: "memory");
-}
-
-// Barrier once the oldest stage in flight has landed, `later` younger stages (each kPer load
-// instructions of this wave) being allowed to stay in flight.
-template <int kPer, int kMaxLater>
-__device__ __forceinline__ void wait_stage(int later) {
-  if constexpr (kMaxLater >= 2) {
-    if (later >= 2) {
-      wait_vm_and_barrier<2 * kPer>();
-      return;
-    }
-  }
-  if constexpr (kMaxLater >= 1) {
-    if (later >= 1) {
-      wait_vm_and_barrier<kPer>();
-      return;
-    }
-  }
-  wait_vm_and_barrier<0>();
 }
 
 // Partial statistics of one lane's column over TM 32-row MFMA blocks.  Element (tm, r) of the
@@ -474,137 +446,6 @@ __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], i
     }
   return Partial{m, (sc[0] + sc[1]) + (sc[2] + sc[3]), (tc[0] + tc[1]) + (tc[2] + tc[3]),
                  min(min(ic[0], ic[1]), min(ic[2], ic[3]))};
-}
-
-template <int WN, int BN, int RING, int MINB, bool kTop2>
-__global__ __launch_bounds__(128 * WN, MINB) void lmhead_tile_kernel(
-    const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
-    int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part,
-    float* __restrict__ part2) {
-  constexpr int BM = kTileBM, BK = kTileBK;
-  constexpr int WM = 2, kWaves = WM * WN;
-  constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
-  constexpr int TM = kWaveM / 32, TN = kWaveN / 32;
-  constexpr int kRowB = BK * 2;                   // 64 bytes per LDS row
-  constexpr int kStageBytes = (BM + BN) * kRowB;
-  constexpr int kInst = (BM + BN) / 16;           // 1 KB wave instructions per stage
-  constexpr int kInstPerWave = kInst / kWaves;
-  static_assert(kInst % kWaves == 0, "stage splits over the waves");
-  static_assert(RING >= 3 && RING <= 4, "ring of 3 or 4 stages");
-  static_assert((RING - 2) * kInstPerWave < 64, "vmcnt range");
-  __shared__ __attribute__((aligned(16))) uint8_t smem[RING * kStageBytes];
-  static_assert(WM * BN * sizeof(Partial) <= RING * kStageBytes, "reduction fits in the ring");
-
-  const int id = blockIdx.x;
-  const int xcd = id % kXcds, k = id / kXcds;
-  const int per_band = kBand * n_rtiles;
-  const int band = xcd + kXcds * (k / per_band);
-  if (band >= n_bands) return;
-  const int tt = k % per_band;
-  const int nv = min(kBand, n_vtiles - band * kBand);
-  if (tt >= nv * n_rtiles) return;
-  const int vt = band * kBand + tt % nv;
-  const int rt = tt / nv;
-  const int v0 = vt * BM, r0 = rt * BN;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave % WM, wn = wave / WM;
-  const int half = lane >> 5, l32 = lane & 31;
-
-  // This wave's load instructions: q = wave * kInstPerWave + i covers tile rows 16 q .. 16 q + 15
-  // (rows below BM are W, the rest h).  Lane L fetches row 16 q + L / 4, global chunk
-  // (L % 4) ^ swizzle(row), so that LDS slot L % 4 of the row holds that chunk.  Rows past the
-  // end are clamped (their products are discarded).
-  const uint16_t* src[kInstPerWave];
-#pragma unroll
-  for (int i = 0; i < kInstPerWave; ++i) {
-    const int q = wave * kInstPerWave + i;
-    const int row = 16 * q + (lane >> 2);
-    const int chunk = (lane & 3) ^ ((row >> 2) & 3);
-    src[i] = row < BM
-                 ? w + static_cast<size_t>(min(v0 + row, vocab - 1)) * hidden + chunk * 8
-                 : h + static_cast<size_t>(min(r0 + row - BM, n_rows - 1)) * hidden + chunk * 8;
-  }
-  auto issue = [&](int kt) {
-    uint8_t* base = smem + (kt % RING) * kStageBytes;
-#pragma unroll
-    for (int i = 0; i < kInstPerWave; ++i)
-      load_to_lds(src[i] + kt * BK, base + (wave * kInstPerWave + i) * 1024);
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < TN; ++b) acc[a][b] = f32x16{};
-
-  const int nk = hidden / BK;
-#pragma unroll
-  for (int j = 0; j < RING - 1; ++j)
-    if (j < nk) issue(j);
-
-  for (int kt = 0; kt < nk; ++kt) {
-    // stage kt lands; younger stages kt+1 .. may stay in flight
-    wait_stage<kInstPerWave, RING - 2>(min(RING - 2, nk - 1 - kt));
-    // refill the slot that was read during iteration kt - 1 (every wave is past it)
-    if (kt + RING - 1 < nk) issue(kt + RING - 1);
-    const uint8_t* st = smem + (kt % RING) * kStageBytes;
-#pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      const int c = 2 * half + s;  // k-chunk of this MFMA step, the same for both operands
-      bf16x8 a[TM], b[TN];
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        const int r = wm * kWaveM + tm * 32 + l32;
-        a[tm] = *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (c ^ ((r >> 2) & 3)));
-      }
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const int r = BM + wn * kWaveN + tn * 32 + l32;
-        b[tn] = *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (c ^ ((r >> 2) & 3)));
-      }
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32(a[tm], b[tn], acc[tm][tn]);
-    }
-  }
-  __syncthreads();  // every wave is done reading the ring before it holds the reduction
-
-  // Epilogue: per-lane partial for its position column, merged with the other half of the
-  // wave, then with the other vocabulary wave through LDS.
-  Partial* red = reinterpret_cast<Partial*>(smem);  // [WM][BN]
-  float* red2 = reinterpret_cast<float*>(red + WM * BN);
-  static_assert(WM * BN * (sizeof(Partial) + 4) <= sizeof(smem), "reduction fits in LDS");
-  const bool full = v0 + BM <= vocab;
-  const int vbase = v0 + wm * kWaveM + 4 * half;
-#pragma unroll
-  for (int tn = 0; tn < TN; ++tn) {
-    float m2 = kNegBig;
-    Partial p = column_partial<TM, TN, kTop2>(acc, tn, vbase, vocab, full, &m2);
-    if (kTop2) m2 = top2_shfl_merge(p.m, m2, 32);
-    p = partial_xor_merge(p, 32, lane);
-    if (lane < 32) {
-      red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
-      if (kTop2) red2[wm * BN + wn * kWaveN + tn * 32 + l32] = m2;
-    }
-  }
-  __syncthreads();
-  for (int c = tid; c < BN; c += kWaves * 64) {
-    Partial p = red[c];
-    float m2 = kTop2 ? red2[c] : kNegBig;
-#pragma unroll
-    for (int q = 1; q < WM; ++q) {
-      const Partial o = red[q * BN + c];
-      if (kTop2) m2 = top2_merge(p.m, m2, o.m, red2[q * BN + c]);
-      p = partial_merge(p, o);
-    }
-    const int row = r0 + c;
-    if (row < n_rows) {
-      part[static_cast<size_t>(row) * n_vtiles + vt] = p;
-      if (kTop2) part2[static_cast<size_t>(row) * n_vtiles + vt] = m2;
-    }
-  }
 }
 
 // Wait until at most N vector-memory instructions of this wave are outstanding and all of its
@@ -781,39 +622,22 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
   }
 }
 
-// Tile kernel of the large-batch path.  Variant 5 (default): lmhead_tile4_kernel, 256 x 256
-// tiles, 4 waves of 128 x 128, ring of 4 (128 KB LDS, one workgroup per compute unit); batch 64:
-// 9.6 ms.  Variant 2: lmhead_tile_kernel with 8 waves of 128 x 64; 10.55 ms.  Variant 1:
-// 256 x 128 tiles, 4 waves, ring of 3 (72 KB, two workgroups per compute unit); 11.8 ms.
-// Measured and dropped: stages reaching LDS through registers (9.65 ms), 64-column stages with
-// one barrier per 64 MFMAs (10.1 ms), DMA loads spread over both halves of a step (no change);
-// with every operand L2-resident the kernel runs at the same speed, so it is bound by the
-// issue/LDS schedule of one wave per SIMD, not by memory.
-#ifndef EB_TILE_VARIANT
-#define EB_TILE_VARIANT 5
-#endif
-constexpr int kTileBN = EB_TILE_VARIANT == 1 ? 128 : 256;
-static_assert(EB_TILE_VARIANT == 1 || EB_TILE_VARIANT == 2 || EB_TILE_VARIANT == 5,
-              "tile variant");
+// Tile kernel of the large-batch path: lmhead_tile4_kernel, 256 x 256 tiles, 4 waves of
+// 128 x 128, ring of 4 (128 KB LDS, one workgroup per compute unit); batch 64: 9.6 ms.
+// Measured and dropped: 8 waves of 128 x 64 (10.55 ms), 256 x 128 tiles with a ring of 3 at two
+// workgroups per compute unit (11.8 ms), stages reaching LDS through registers (9.65 ms),
+// 64-column stages with one barrier per 64 MFMAs (10.1 ms), DMA loads spread over both halves of
+// a step (no change); with every operand L2-resident the kernel runs at the same speed, so it is
+// bound by the issue/LDS schedule of one wave per SIMD, not by memory.
+constexpr int kTileBN = 256;
 
 template <bool kTop2>
 hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const void* w,
                        Partial* part, float* part2, hipStream_t s) {
   const TileMap m = tile_map(n_rows, vocab, kTileBN);
-  const uint16_t* hp = static_cast<const uint16_t*>(h);
-  const uint16_t* wp = static_cast<const uint16_t*>(w);
-  if constexpr (EB_TILE_VARIANT == 1) {
-    hipLaunchKernelGGL((lmhead_tile_kernel<2, 128, 3, 2, kTop2>), dim3(m.grid), dim3(256), 0, s,
-                       hp, wp, n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part,
-                       part2);
-  } else if constexpr (EB_TILE_VARIANT == 5) {
-    hipLaunchKernelGGL((lmhead_tile4_kernel<4, kTop2>), dim3(m.grid), dim3(256), 0, s, hp, wp,
-                       n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part, part2);
-  } else {
-    hipLaunchKernelGGL((lmhead_tile_kernel<4, 256, 4, 1, kTop2>), dim3(m.grid), dim3(512), 0, s,
-                       hp, wp, n_rows, hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part,
-                       part2);
-  }
+  hipLaunchKernelGGL((lmhead_tile4_kernel<4, kTop2>), dim3(m.grid), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w), n_rows,
+                     hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part, part2);
   return hipGetLastError();
 }
 
