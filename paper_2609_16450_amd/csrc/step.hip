@@ -85,10 +85,11 @@ __global__ __launch_bounds__(kFinishThreads) void step_finish_kernel(
   }
   __syncthreads();  // the block's conf / argmax rows are written before the block step reads them
   if (small) {
-    if (wave == 0)
-      unmask_wave_threshold(b, own_row, own_ok, m_own, own_ok ? s_conf[lane] : 0.f,
-                            own_ok ? s_arg[lane] : 0, tau[b], masked, tokens, unmask, n_commit,
-                            resolved, lane);
+    if (wave == 0) {
+      const float c = own_ok ? s_conf[lane] : 0.f;
+      unmask_wave(b, own_row, own_ok, m_own != 0, c, own_ok ? s_arg[lane] : 0, c >= tau[b],
+                  masked, tokens, unmask, n_commit, resolved, lane);
+    }
     return;
   }
   unmask_block<kThreshold, kFinishThreads>(b, ap.cu_block, conf, argmax, tau,

@@ -78,19 +78,18 @@ __device__ __forceinline__ void rank_rows(int beg, int end, const float* __restr
   }
 }
 
-// Threshold step of a block of at most 64 rows by one wavefront (the rule, tie-break and commit
-// of unmask_block<kThreshold>): lane l holds row `row` (valid when `mine`), its mask flag m, its
-// conf c and its top-1 token x; tb is the block's tau.
-__device__ __forceinline__ void unmask_wave_threshold(int b, int row, bool mine, uint8_t m,
-                                                      float c, int32_t x, float tb,
-                                                      uint8_t* __restrict__ masked,
-                                                      int32_t* __restrict__ tokens,
-                                                      uint8_t* __restrict__ unmask,
-                                                      int32_t* __restrict__ n_commit,
-                                                      uint8_t* __restrict__ resolved, int lane) {
+// Block step of a block of at most 64 rows by one wavefront (the commit, fallback and tie-break
+// of unmask_block): lane l holds row `row` (valid when `mine`), its mask flag m, its conf c, its
+// top-1 token x, and whether it passes the accept rule.
+__device__ __forceinline__ void unmask_wave(int b, int row, bool mine, bool m, float c, int32_t x,
+                                            bool pass, uint8_t* __restrict__ masked,
+                                            int32_t* __restrict__ tokens,
+                                            uint8_t* __restrict__ unmask,
+                                            int32_t* __restrict__ n_commit,
+                                            uint8_t* __restrict__ resolved, int lane) {
   const bool mk = mine && m;
   int n_masked = mk ? 1 : 0;
-  int n_pass = (mk && c >= tb) ? 1 : 0;
+  int n_pass = (mk && pass) ? 1 : 0;
   Best best = mk ? Best{c, row} : Best{-INFINITY, kNoIndex};
   for (int mask = 32; mask >= 1; mask >>= 1) {
     n_masked += __shfl_xor(n_masked, mask);
@@ -100,7 +99,7 @@ __device__ __forceinline__ void unmask_wave_threshold(int b, int row, bool mine,
   }
   const bool use_rule = n_pass > 0;
   if (mine) {
-    const bool take = mk && (use_rule ? c >= tb : row == best.i);
+    const bool take = mk && (use_rule ? pass : row == best.i);
     unmask[row] = take ? 1 : 0;
     if (take) {
       tokens[row] = x;
@@ -131,6 +130,19 @@ __device__ __forceinline__ void unmask_block(
   const float tb = tau[b];
 
   if constexpr (R != kTopM) {
+    if (end - beg <= 64) {  // one wavefront: no reduction across waves, no barrier
+      if (wave == 0) {
+        const int i = beg + lane;
+        const bool mine = i < end;
+        const bool m = mine && masked[i];
+        const float c = mine ? conf[i] : 0.f;
+        const int32_t x = mine ? argmax[i] : 0;
+        bool pass = c >= tb;
+        if constexpr (R == kUnion) pass = pass || (mine && ra.p_psi[i] > ra.tau_psi);
+        unmask_wave(b, i, mine, m, c, x, pass, masked, tokens, unmask, n_commit, resolved, lane);
+      }
+      return;
+    }
     // One pass counts the masked rows, finds the best masked row and counts the rows passing
     // the rule.  Each thread then decides and commits its own rows: the rule reads no other
     // row's mask flag, so a row is committed as soon as it is decided.
