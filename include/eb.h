@@ -26,7 +26,11 @@
  *     of the calling thread.
  *   - Device-array contents are the caller's contract and are not checked: cu arrays are
  *     non-decreasing, start at 0 and end at the totals given on the host, maxima are
- *     true maxima, tau lies in (0, 1], inputs are finite.
+ *     true maxima, tau lies in (0, 1], inputs are finite.  For debugging, the environment
+ *     variable EB_DEBUG_CHECKS (any value but "0") makes every entry point that takes cu
+ *     arrays or tau copy them to the host after the work already on its stream (which
+ *     synchronises that stream) and return EB_ERR_INVALID, launching nothing, when they break
+ *     this contract.  Such calls cannot be captured in a graph.
  *   - Rows are packed: the block rows of sequence b are rows cu_block[b] .. cu_block[b+1]-1,
  *     in ascending sequence position (a non-contiguous block is gathered in order), its
  *     cached prefix rows are cu_prefix[b] .. cu_prefix[b+1]-1.  Empty blocks are legal.

@@ -4,7 +4,11 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <stdlib.h>
+#include <string.h>
+
 #include <string>
+#include <vector>
 
 #include "../../include/eb.h"
 #include "eb_internal.hpp"
@@ -109,6 +113,65 @@ eb_status check_unmask(const eb_ragged* r, const void* conf, const void* argmax,
   return EB_OK;
 }
 
+// ---- optional checks of the device-array contract --------------------------------------
+// With the environment variable EB_DEBUG_CHECKS set (to anything but "0"), an entry point copies
+// its offset arrays (and tau) to the host after the work already on `stream`, and returns
+// EB_ERR_INVALID, launching nothing, when they break the contract stated in eb.h.  The copy
+// synchronises the stream, so these checks are for debugging, not for captured or timed code.
+bool debug_checks() {
+  const char* v = getenv("EB_DEBUG_CHECKS");
+  return v && *v && strcmp(v, "0") != 0;
+}
+
+template <class T>
+eb_status fetch(std::vector<T>& h, const T* d, int n, hipStream_t s) {
+  h.resize(n);
+  hipError_t e = hipMemcpyAsync(h.data(), d, sizeof(T) * n, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  return e == hipSuccess ? EB_OK : fail(EB_ERR_HIP, "debug check copy: %s", hipGetErrorString(e));
+}
+
+// cu [batch + 1]: starts at 0, non-decreasing, ends at `total`, largest step `max`.
+eb_status check_cu(const char* name, const int32_t* cu, int batch, int total, int max,
+                   hipStream_t s) {
+  std::vector<int32_t> h;
+  eb_status st = fetch(h, cu, batch + 1, s);
+  if (st != EB_OK) return st;
+  if (h[0] != 0) return fail(EB_ERR_INVALID, "%s[0] = %d, expected 0", name, h[0]);
+  int mx = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (h[b + 1] < h[b])
+      return fail(EB_ERR_INVALID, "%s decreases at %d (%d -> %d)", name, b, h[b], h[b + 1]);
+    mx = h[b + 1] - h[b] > mx ? h[b + 1] - h[b] : mx;
+  }
+  if (h[batch] != total)
+    return fail(EB_ERR_INVALID, "%s[%d] = %d but the host total is %d", name, batch, h[batch],
+                total);
+  if (mx != max)
+    return fail(EB_ERR_INVALID, "largest %s step is %d but the host maximum is %d", name, mx, max);
+  return EB_OK;
+}
+
+eb_status check_tau(const float* tau, int batch, hipStream_t s) {
+  std::vector<float> h;
+  eb_status st = fetch(h, tau, batch, s);
+  if (st != EB_OK) return st;
+  for (int b = 0; b < batch; ++b)
+    if (!(h[b] > 0.f && h[b] <= 1.f))
+      return fail(EB_ERR_INVALID, "tau[%d] = %g is not in (0, 1]", b, (double)h[b]);
+  return EB_OK;
+}
+
+// The ragged descriptor's arrays (cu_prefix too when need_prefix) and, when given, tau.
+eb_status check_device(const eb_ragged* r, bool need_prefix, const float* tau, hipStream_t s) {
+  if (!debug_checks()) return EB_OK;
+  eb_status st = check_cu("cu_block", r->cu_block, r->batch, r->total_block, r->max_block, s);
+  if (st == EB_OK && need_prefix)
+    st = check_cu("cu_prefix", r->cu_prefix, r->batch, r->total_prefix, r->max_prefix, s);
+  if (st == EB_OK && tau) st = check_tau(tau, r->batch, s);
+  return st;
+}
+
 }  // namespace
 
 extern "C" {
@@ -144,6 +207,8 @@ eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int he
   const size_t need = eb_block_attn_workspace(dt, r, hq, hkv, head_dim);
   if (ws_bytes < need || (need && !ws))
     return fail(EB_ERR_WORKSPACE, "attention workspace %zu bytes < required %zu", ws_bytes, need);
+  st = check_device(r, true, nullptr, stream);
+  if (st != EB_OK) return st;
   eb::AttnArgs a{r->batch, r->total_block, r->max_block, r->total_prefix, r->max_prefix,
                  r->cu_block, r->cu_prefix, hq, hkv, head_dim, scale, q, k_blk, v_blk,
                  k_pre, v_pre, out};
@@ -178,6 +243,11 @@ eb_status eb_block_attn_dual(eb_dtype dt, const eb_ragged* r, const eb_suffix* s
   const size_t need = eb_block_attn_dual_workspace(dt, r, sfx, hq, hkv, head_dim);
   if (ws_bytes < need || (need && !ws))
     return fail(EB_ERR_WORKSPACE, "attention workspace %zu bytes < required %zu", ws_bytes, need);
+  st = check_device(r, true, nullptr, stream);
+  if (st == EB_OK && debug_checks())
+    st = check_cu("cu_suffix", sfx->cu_suffix, r->batch, sfx->total_suffix, sfx->max_suffix,
+                  stream);
+  if (st != EB_OK) return st;
   eb::AttnArgs a{r->batch, r->total_block, r->max_block, r->total_prefix, r->max_prefix,
                  r->cu_block, r->cu_prefix, hq, hkv, head_dim, scale, q, k_blk, v_blk,
                  k_pre, v_pre, out, sfx->max_suffix, sfx->cu_suffix, k_suf, v_suf};
@@ -247,6 +317,8 @@ eb_status eb_lps_features(const eb_ragged* r, int vocab, const float* conf,
     return fail(EB_ERR_INVALID, "NULL conf / entropy / top2_gap / masked / feat / pos");
   if (r->total_block > 0 && !aligned16(feat))
     return fail(EB_ERR_INVALID, "feat must be 16-byte aligned");
+  st = check_device(r, false, nullptr, stream);
+  if (st != EB_OK) return st;
   return hip_status(eb::lps_features(r->batch, r->cu_block, vocab, conf, entropy_nats, top2_gap,
                                      masked, feat, pos, mask_ratio, stream),
                     "eb_lps_features launch");
@@ -259,6 +331,8 @@ eb_status eb_unmask_select_lps(const eb_ragged* r, const float* conf, const int3
   eb_status st = check_unmask(r, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved);
   if (st != EB_OK) return st;
   if (r->total_block > 0 && !p_psi) return fail(EB_ERR_INVALID, "NULL p_psi");
+  st = check_device(r, false, tau, stream);
+  if (st != EB_OK) return st;
   return hip_status(eb::unmask_select_lps(r->batch, r->cu_block, conf, argmax, tau, p_psi,
                                           tau_psi, masked, tokens, unmask, n_commit, resolved,
                                           stream),
@@ -272,6 +346,8 @@ eb_status eb_unmask_select_topm(const eb_ragged* r, const float* conf, const int
   eb_status st = check_unmask(r, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved);
   if (st != EB_OK) return st;
   if (m < 0) return fail(EB_ERR_INVALID, "m must be >= 0 (got %d)", m);
+  st = check_device(r, false, tau, stream);
+  if (st != EB_OK) return st;
   return hip_status(eb::unmask_select_topm(r->batch, r->cu_block, conf, argmax, tau, m, masked,
                                            tokens, unmask, n_commit, resolved, stream),
                     "eb_unmask_select_topm launch");
@@ -281,6 +357,8 @@ eb_status eb_unmask_select(const eb_ragged* r, const float* conf, const int32_t*
                            const float* tau, uint8_t* masked, int32_t* tokens, uint8_t* unmask,
                            int32_t* n_commit, uint8_t* resolved, eb_stream_t stream) {
   eb_status st = check_unmask(r, conf, argmax, tau, masked, tokens, unmask, n_commit, resolved);
+  if (st != EB_OK) return st;
+  st = check_device(r, false, tau, stream);
   if (st != EB_OK) return st;
   return hip_status(eb::unmask_select(r->batch, r->max_block, r->cu_block, conf, argmax, tau,
                                       masked, tokens, unmask, n_commit, resolved, stream),
@@ -327,6 +405,8 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
   const size_t need = eb_decode_step_workspace(d);
   if (ws_bytes < need || (need && !ws))
     return fail(EB_ERR_WORKSPACE, "step workspace %zu bytes < required %zu", ws_bytes, need);
+  st = check_device(&d->ragged, true, d->tau, stream);
+  if (st != EB_OK) return st;
 
   const bool bf16 = d->dtype == EB_BF16;
   const eb_ragged* r = &d->ragged;

@@ -8,6 +8,7 @@ Bars (written here, enforced below):
   * attention output: bf16 within rtol 2e-2 / atol 2e-2, fp32 within 1e-4.
 """
 import math
+import os
 import sys
 
 import numpy as np
@@ -457,3 +458,58 @@ def test_decode_step_random_shapes(i):
         ref = oracle.block_attention(**f, cu_block=case.cu_block, cu_prefix=case.cu_prefix,
                                      hq=spec["hq"], hkv=spec["hkv"])
         np.testing.assert_allclose(attn_out_f32(a.attn_out), ref, **ATTN_TOL_BF16)
+
+
+class _DebugChecks:
+    """EB_DEBUG_CHECKS=1 for the duration of a with-block."""
+
+    def __enter__(self):
+        self.old = os.environ.get("EB_DEBUG_CHECKS")
+        os.environ["EB_DEBUG_CHECKS"] = "1"
+
+    def __exit__(self, *exc):
+        if self.old is None:
+            os.environ.pop("EB_DEBUG_CHECKS", None)
+        else:
+            os.environ["EB_DEBUG_CHECKS"] = self.old
+
+
+def test_debug_checks_reject_bad_device_arrays():
+    # With EB_DEBUG_CHECKS set, entry points check the device offset arrays and tau against the
+    # contract on the host and launch nothing when they break it.  Every bad array below keeps
+    # all row indices inside [0, T), so no kernel could read out of bounds even unchecked.
+    say("debug checks of the device-array contract")
+    from paper_2609_16450_amd import EbError
+    T, B = 32, 2
+    dev = lambda x, dt: torch.tensor(x, dtype=dt, device="cuda")
+    conf = dev(np.linspace(0.1, 0.95, T), torch.float32)
+    argmax = dev(np.arange(T), torch.int32)
+    masked = torch.ones(T, dtype=torch.uint8, device="cuda")
+    tokens = torch.full((T,), -1, dtype=torch.int32, device="cuda")
+    unmask = torch.empty(T, dtype=torch.uint8, device="cuda")
+    n_commit = torch.empty(B, dtype=torch.int32, device="cuda")
+    resolved = torch.empty(B, dtype=torch.uint8, device="cuda")
+    tau = dev([0.9, 0.9], torch.float32)
+    zero = dev([0, 0, 0], torch.int32)
+    rag = lambda cu: Ragged(B, T, 20, 0, 0, dev(cu, torch.int32), zero)
+    run = lambda r, t: eb_unmask_select(r, conf, argmax, t, masked, tokens, unmask, n_commit,
+                                        resolved)
+    with _DebugChecks():
+        run(rag([0, 20, 32]), tau)  # a valid call passes the checks
+        torch.cuda.synchronize()
+        for cu, what in (([0, 20, 12], "decreases"), ([0, 16, 30], "host total"),
+                         ([2, 16, 32], "expected 0"), ([0, 10, 32], "host maximum")):
+            with pytest.raises(EbError) as err:
+                run(rag(cu), tau)
+            assert "EB_ERR_INVALID" in str(err.value) and what in str(err.value), err.value
+        with pytest.raises(EbError) as err:
+            run(rag([0, 20, 32]), dev([0.0, 0.9], torch.float32))
+        assert "tau[0]" in str(err.value)
+        # attention: a prefix offset array that does not end at the host total
+        r = Ragged(1, 8, 8, 40, 40, dev([0, 8], torch.int32), dev([0, 39], torch.int32))
+        x = torch.zeros(8, 4, 64, dtype=torch.bfloat16, device="cuda")
+        kv = torch.zeros(40, 4, 64, dtype=torch.bfloat16, device="cuda")
+        with pytest.raises(EbError) as err:
+            eb_block_attn(r, x, x, x, kv, kv, torch.empty_like(x))
+        assert "cu_prefix" in str(err.value)
+    torch.cuda.synchronize()
