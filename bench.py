@@ -132,6 +132,34 @@ def timed(torch, stream, steps, run):
     return (time.perf_counter() - t0) * 1e3 / steps
 
 
+def measured_peaks(torch) -> dict:
+    """Same-box reference rates beside the spec peaks: a 1 GiB device-to-device copy (read +
+    write bytes per second) and a bf16 8192^3 GEMM through torch's library path."""
+    def ev_ms(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    copy_ms = ev_ms(lambda: dst.copy_(src), 10)
+    del src, dst
+    k = 8192
+    x = torch.randn(k, k, device="cuda:0").to(torch.bfloat16)
+    y = torch.randn(k, k, device="cuda:0").to(torch.bfloat16)
+    gemm_ms = ev_ms(lambda: torch.mm(x, y), 10)
+    del x, y
+    return {"copy_GBps": 2 * n / (copy_ms * 1e-3) / 1e9,
+            "gemm_bf16_TFLOPs": 2.0 * k ** 3 / (gemm_ms * 1e-3) / 1e12,
+            "note": "1 GiB device copy (read + write), bf16 8192^3 torch.mm; same box, same run"}
+
+
 def variant_leg(args, torch, eb, case, copies, stream) -> int:
     """The next-row paths: one JSON line with the same fields as the headline."""
     from workloads import lbs_window, router_scores, suffix_segment
@@ -375,6 +403,8 @@ def main() -> int:
                      "kernel_us": lm_ms * 1e3, "algorithmic_bytes": nbytes,
                      "algorithmic_flops": flops},
     }
+    result["roofline"]["measured_peak"] = measured_peaks(torch)
+    log(f"bench: measured peaks {result['roofline']['measured_peak']}")
     if not args.no_cpu_baseline:
         log("bench: timing the fp64 oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(case)
