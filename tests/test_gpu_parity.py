@@ -71,6 +71,12 @@ LM_CASES = [
     (2, 64, 262144, "bf16"),
     (40, 1600, 9000, "bf16"),
     (3, 4160, 20000, "bf16"),
+    # extremes: a one- and a two-entry vocabulary (both kernels), a hidden size of 8192
+    (4, 64, 1, "bf16"),
+    (70, 64, 1, "bf16"),
+    (3, 64, 2, "bf16"),
+    (16, 8192, 3000, "bf16"),
+    (130, 8192, 2000, "bf16"),
     (32, 256, 2048, "f32"),
     (7, 100, 999, "f32"),
 ]
