@@ -400,23 +400,25 @@ __device__ __forceinline__ void load_to_lds(const void* g, void* l) {
 }
 
 // Partial statistics of one lane's column over TM 32-row MFMA blocks.  Element (tm, r) of the
-// lane is vocabulary row vbase + 32 tm + 8 (r / 4) + (r % 4).  Four independent chains (by
-// r % 4) carry the max, the sums and the first argmax, so the reduction is not bound by the
+// lane is vocabulary row vbase + o with o = 32 tm + 8 (r / 4) + (r % 4).  Four independent chains
+// (by r % 4) carry the max, the sums and the first argmax, so the reduction is not bound by the
 // latency of one long dependency chain; each chain walks its rows in decreasing order, so its
-// last z == max hit is its lowest row, and the chains are combined at the end.
-// With kTop2 the max pass also tracks each chain's second-largest logit; m2 returns the
-// lane's second-largest (kNegBig if none).
-template <int TM, int TN, bool kTop2 = false>
+// last z == max hit is its lowest row, and the chains are combined at the end.  The argmax is
+// tracked as the offset o, a constant of the unrolled code, and kFull (every row inside the
+// vocabulary) drops the per-row bounds test: neither a row index nor a mask is then kept per
+// element.  With kTop2 the max pass also tracks each chain's second-largest logit; m2 returns
+// the lane's second-largest (kNegBig if none).
+template <int TM, int TN, bool kTop2, bool kFull>
 __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], int tn, int vbase,
-                                                  int vocab, bool full, float* m2 = nullptr) {
+                                                  int vocab, float* m2) {
   float mc[4] = {kNegBig, kNegBig, kNegBig, kNegBig};
   float mc2[4] = {kNegBig, kNegBig, kNegBig, kNegBig};
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int v = vbase + tm * 32 + 8 * (r >> 2) + (r & 3);
-      if (full || v < vocab) {
+      const int o = tm * 32 + 8 * (r >> 2) + (r & 3);
+      if (kFull || vbase + o < vocab) {
         const float z = acc[tm][tn][r];
         // with mc >= mc2, the new second-largest is the median of (mc, mc2, z): one v_med3
         if (kTop2) mc2[r & 3] = __builtin_amdgcn_fmed3f(mc[r & 3], mc2[r & 3], z);
@@ -428,24 +430,41 @@ __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], i
     *m2 = top2_merge(fmaxf(mc[0], mc[1]), top2_merge(mc[0], mc2[0], mc[1], mc2[1]),
                      fmaxf(mc[2], mc[3]), top2_merge(mc[2], mc2[2], mc[3], mc2[3]));
   float sc[4] = {0.f, 0.f, 0.f, 0.f}, tc[4] = {0.f, 0.f, 0.f, 0.f};
-  int32_t ic[4] = {kNoIndex, kNoIndex, kNoIndex, kNoIndex};
+  int32_t oc[4] = {kNoIndex, kNoIndex, kNoIndex, kNoIndex};
 #pragma unroll
   for (int tm = TM - 1; tm >= 0; --tm)
 #pragma unroll
     for (int r = 15; r >= 0; --r) {
-      const int v = vbase + tm * 32 + 8 * (r >> 2) + (r & 3);
+      const int o = tm * 32 + 8 * (r >> 2) + (r & 3);
       const float z = acc[tm][tn][r];
-      const bool ok = full || v < vocab;
-      // rows past the vocabulary contribute e = 0 and y = 0 (a lane with no valid row keeps
-      // m = kNegBig, where z - m would overflow and 0 * inf would poison t)
-      const float y = ok ? (z - m) * kLog2e : 0.f;
-      const float e = ok ? fast_exp2(y) : 0.f;
-      sc[r & 3] += e;
-      tc[r & 3] = fmaf(e, y, tc[r & 3]);
-      ic[r & 3] = (ok && z == m) ? v : ic[r & 3];
+      if (kFull) {
+        const float y = (z - m) * kLog2e;
+        const float e = fast_exp2(y);
+        sc[r & 3] += e;
+        tc[r & 3] = fmaf(e, y, tc[r & 3]);
+        oc[r & 3] = z == m ? o : oc[r & 3];
+      } else {
+        const bool ok = vbase + o < vocab;
+        // rows past the vocabulary contribute e = 0 and y = 0 (a lane with no valid row keeps
+        // m = kNegBig, where z - m would overflow and 0 * inf would poison t)
+        const float y = ok ? (z - m) * kLog2e : 0.f;
+        const float e = ok ? fast_exp2(y) : 0.f;
+        sc[r & 3] += e;
+        tc[r & 3] = fmaf(e, y, tc[r & 3]);
+        oc[r & 3] = (ok && z == m) ? o : oc[r & 3];
+      }
     }
+  const int32_t ob = min(min(oc[0], oc[1]), min(oc[2], oc[3]));
   return Partial{m, (sc[0] + sc[1]) + (sc[2] + sc[3]), (tc[0] + tc[1]) + (tc[2] + tc[3]),
-                 min(min(ic[0], ic[1]), min(ic[2], ic[3]))};
+                 ob == kNoIndex ? kNoIndex : vbase + ob};
+}
+
+// column_partial with the bounds test only where the tile reaches past the vocabulary.
+template <int TM, int TN, bool kTop2>
+__device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], int tn, int vbase,
+                                                  int vocab, bool full, float* m2) {
+  return full ? column_partial<TM, TN, kTop2, true>(acc, tn, vbase, vocab, m2)
+              : column_partial<TM, TN, kTop2, false>(acc, tn, vbase, vocab, m2);
 }
 
 // Wait until at most N vector-memory instructions of this wave are outstanding and all of its
