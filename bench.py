@@ -294,6 +294,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 3 device-to-device copies of BYTES (calibrates HBM counters)")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the same-box copy and GEMM reference rates (e.g. under a profiler)")
     ap.add_argument("--path", default="step", choices=["step", "lps", "topm", "dual", "lbs"],
                     help="step: eb_decode_step (the headline); lps: attention + LM head with the "
                          "top-2 gap + LPS features + union accept rule; topm: attention + LM head "
@@ -403,8 +405,9 @@ def main() -> int:
                      "kernel_us": lm_ms * 1e3, "algorithmic_bytes": nbytes,
                      "algorithmic_flops": flops},
     }
-    result["roofline"]["measured_peak"] = measured_peaks(torch)
-    log(f"bench: measured peaks {result['roofline']['measured_peak']}")
+    if not args.no_peaks:
+        result["roofline"]["measured_peak"] = measured_peaks(torch)
+        log(f"bench: measured peaks {result['roofline']['measured_peak']}")
     if not args.no_cpu_baseline:
         log("bench: timing the fp64 oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(case)
