@@ -8,6 +8,8 @@
 // bf16 path: scores are computed transposed, S^T = K Q^T, so each lane owns one query row
 // (an MFMA column) and reduces its softmax statistics in registers; the probabilities then
 // feed P V directly as the B operand of O^T = V^T P^T, with V staged transposed in LDS.
+// Small steps (attn_small_ok) take the 16-row role of attn_small.hpp instead, here as a kernel
+// of its own; the decode step runs the same role inside the LM-head launch.
 #include "attn_common.hpp"
 #include "attn_small.hpp"
 #include "eb_common.hpp"

@@ -1,13 +1,14 @@
 // Fused epilogue of one decoding step (Alg. 5, one loop iteration, after the attention and the
-// LM-head partials): a single launch that
+// LM-head partials, which in small steps come from one launch): a single launch that
 //   * merges the attention key-split partials of every (block row, query head) pair, and
 //   * per block: merges each row's LM-head partials into conf, entropy, argmax and top logit
 //     (Alg. 5, confidence of the softmax), then applies the threshold unmask with the
 //     anti-stall fallback (Eq. prelim-update, Alg. 5).
 // The two roles touch disjoint data, so they share one grid: workgroups [0, n_merge) merge
 // attention pairs, the next `batch` workgroups each finish one block.  Each block's rows are
-// reduced by the block's own workgroup, whose unmask step then reads them back after a barrier,
-// so no cross-workgroup ordering is needed.  The arithmetic is that of the separate kernels
+// reduced by the block's own workgroup, whose unmask step then reads them back after a barrier
+// (a block of at most 64 rows: from LDS, by one wavefront), so no cross-workgroup ordering is
+// needed.  The arithmetic is that of the separate kernels
 // (same partial merge order, same row statistics, same block step), so the outputs are
 // bit-identical to attention merge + combine + unmask launched one after another.
 #include "attn_common.hpp"
