@@ -320,6 +320,12 @@ typedef struct {
 size_t eb_decode_step_workspace(const eb_step_desc* d);
 eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_stream_t stream);
 
+/* 1 when eb_decode_step with this descriptor runs the attention's workgroups inside the LM-head
+ * launch (the small-step case above), else 0 (also for a NULL descriptor).  Reads only the
+ * descriptor's host fields (dtype, ragged sizes, heads, head_dim, vocab); launches nothing.  For
+ * profilers that attribute the shared launch's time and bytes. */
+int32_t eb_decode_step_attn_in_lmhead(const eb_step_desc* d);
+
 /* ---------------------------------------------------------------------------------------
  * Diagnostics.
  * ------------------------------------------------------------------------------------- */

@@ -87,6 +87,7 @@ EXPORTS = {
                                      _P]),
     "eb_decode_step_workspace": (ctypes.c_size_t, [ctypes.POINTER(eb_step_desc)]),
     "eb_decode_step": (ctypes.c_int, [ctypes.POINTER(eb_step_desc), _P, ctypes.c_size_t, _P]),
+    "eb_decode_step_attn_in_lmhead": (ctypes.c_int32, [ctypes.POINTER(eb_step_desc)]),
     "eb_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "eb_last_error": (ctypes.c_char_p, []),
     "eb_version": (ctypes.c_char_p, []),
@@ -476,6 +477,11 @@ class StepBuffers:
 
 def eb_decode_step_workspace(buffers: StepBuffers) -> int:
     return int(load().eb_decode_step_workspace(ctypes.byref(buffers.desc)))
+
+
+def eb_decode_step_attn_in_lmhead(buffers: StepBuffers) -> bool:
+    """Whether eb_decode_step runs the attention inside the LM-head launch for these buffers."""
+    return bool(load().eb_decode_step_attn_in_lmhead(ctypes.byref(buffers.desc)))
 
 
 def eb_decode_step(buffers: StepBuffers, stream=None, trace: Optional[eb_step_trace] = None) -> None:

@@ -383,6 +383,21 @@ eb_status eb_lbs_select(int32_t n_seq, int32_t window, const uint8_t* masked,
                     "eb_lbs_select launch");
 }
 
+int32_t eb_decode_step_attn_in_lmhead(const eb_step_desc* d) {
+  if (!d || d->hkv < 1 || d->hq < 1) return 0;
+  const eb_ragged* r = &d->ragged;
+  const bool bf16 = d->dtype == EB_BF16;
+  const int T = r->total_block;
+  eb::AttnArgs a{r->batch, T, r->max_block, r->total_prefix, r->max_prefix, r->cu_block,
+                 r->cu_prefix, d->hq, d->hkv, d->head_dim, 1.0f, d->q, d->k_blk, d->v_blk,
+                 d->k_pre, d->v_pre, d->attn_out};
+  const int n_slices = T > 0 && d->vocab > 0 ? eb::lmhead_num_slices(bf16, T, d->vocab) : 0;
+  return eb::step_finish_fusable(r->max_block, n_slices) &&
+                 eb::lmhead_hosts_attn(bf16, T, d->vocab, a)
+             ? 1
+             : 0;
+}
+
 size_t eb_decode_step_workspace(const eb_step_desc* d) {
   if (!d) return 0;
   return eb_block_attn_workspace(d->dtype, &d->ragged, d->hq, d->hkv, d->head_dim) +
@@ -426,7 +441,7 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
 
   // Small steps: the attention's workgroups ride in the LM-head launch, behind its slices (its
   // split merge then happens in the epilogue, which is why this needs `fuse`).
-  const bool hosted = fuse && eb::lmhead_hosts_attn(bf16, T, d->vocab, a);
+  const bool hosted = eb_decode_step_attn_in_lmhead(d) != 0;
 
   hipError_t e = tr ? mark(tr->attn_begin) : hipSuccess;
   if (e == hipSuccess && !hosted) e = eb::block_attn(bf16, true, a, ws, stream, fuse);

@@ -120,3 +120,25 @@ def test_status_strings():
     assert B.eb_status_string(0) == "EB_OK"
     assert B.eb_status_string(3) == "EB_ERR_WORKSPACE"
     assert "gfx950" in B.eb_version()
+
+
+def test_attention_in_lmhead_query():
+    # Host-only query: which decode steps run the attention inside the LM-head launch.
+    lib = B.load()
+
+    def desc(dtype, batch, total, max_block, hq, hkv, head_dim, vocab):
+        d = B.eb_step_desc()
+        d.dtype = dtype
+        d.ragged = B.eb_ragged(batch, total, max_block, 512 * batch, 512, 0x1000, 0x2000)
+        d.hq, d.hkv, d.head_dim, d.hidden, d.vocab = hq, hkv, head_dim, 4096, vocab
+        return ctypes.byref(d)
+
+    q = lib.eb_decode_step_attn_in_lmhead
+    assert q(None) == 0
+    assert q(desc(B.EB_BF16, 1, 32, 32, 32, 32, 128, 126464)) == 1   # batch-1 LLaDA shape
+    assert q(desc(B.EB_BF16, 1, 64, 64, 16, 4, 64, 20000)) == 1      # 256 query rows per head
+    assert q(desc(B.EB_BF16, 1, 65, 65, 4, 4, 128, 20000)) == 0      # more than 64 block rows
+    assert q(desc(B.EB_BF16, 1, 40, 40, 28, 4, 128, 20000)) == 0     # 280 query rows per head
+    assert q(desc(B.EB_BF16, 1, 16, 16, 4, 4, 128, 262144)) == 0     # 8-wave LM-head launch
+    assert q(desc(B.EB_F32, 1, 32, 32, 4, 4, 64, 2048)) == 0          # fp32 path
+    assert q(desc(B.EB_BF16, 2, 0, 0, 4, 4, 128, 2048)) == 0          # no block rows
