@@ -311,7 +311,7 @@ def main() -> int:
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the step is built and timed on a single MI355X "
-              "(sharding across GPUs is a design note, not part of this build).", file=sys.stderr)
+              "(how the step would shard across GPUs is a design note only).", file=sys.stderr)
         return 2
 
     import torch
