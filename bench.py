@@ -138,9 +138,10 @@ def timed(torch, stream, steps, run):
     return (time.perf_counter() - t0) * 1e3 / steps
 
 
-def measured_peaks(torch) -> dict:
+def measured_peaks(torch, eb) -> dict:
     """Same-box reference rates beside the spec peaks: a 1 GiB device-to-device copy (read +
-    write bytes per second) and a bf16 8192^3 GEMM through torch's library path."""
+    write bytes per second), a bf16 8192^3 GEMM through torch's library path and the library's
+    register-only bf16 MFMA loop (the matrix-core rate at the clock the chip holds under load)."""
     def ev_ms(fn, reps):
         fn()
         torch.cuda.synchronize()
@@ -161,9 +162,17 @@ def measured_peaks(torch) -> dict:
     y = torch.randn(k, k, device="cuda:0").to(torch.bfloat16)
     gemm_ms = ev_ms(lambda: torch.mm(x, y), 10)
     del x, y
+    groups, iters = 4096, 4096
+    out = torch.empty(groups * 256, dtype=torch.float32, device="cuda:0")
+    flops = eb.eb_probe_mfma_bf16(out, groups, iters)
+    mfma_ms = ev_ms(lambda: eb.eb_probe_mfma_bf16(out, groups, iters), 5)
+    del out
     return {"copy_GBps": 2 * n / (copy_ms * 1e-3) / 1e9,
             "gemm_bf16_TFLOPs": 2.0 * k ** 3 / (gemm_ms * 1e-3) / 1e12,
-            "note": "1 GiB device copy (read + write), bf16 8192^3 torch.mm; same box, same run"}
+            "mfma_loop_bf16_TFLOPs": flops / (mfma_ms * 1e-3) / 1e12,
+            "note": ("1 GiB device copy (read + write), bf16 8192^3 torch.mm, register-only bf16 "
+                     "32x32x16 MFMA loop (eb_probe_mfma_bf16, 4096 groups x 4096 iterations); "
+                     "same box, same run")}
 
 
 def variant_leg(args, torch, eb, case, copies, stream) -> int:
@@ -417,7 +426,7 @@ def main() -> int:
                      "algorithmic_flops": flops},
     }
     if not args.no_peaks:
-        result["roofline"]["measured_peak"] = measured_peaks(torch)
+        result["roofline"]["measured_peak"] = measured_peaks(torch, eb)
         log(f"bench: measured peaks {result['roofline']['measured_peak']}")
     if not args.no_cpu_baseline:
         log("bench: timing the fp64 oracle on a bounded sample")

@@ -327,6 +327,22 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
 int32_t eb_decode_step_attn_in_lmhead(const eb_step_desc* d);
 
 /* ---------------------------------------------------------------------------------------
+ * Measurement aid (not part of the denoising step).
+ *
+ * A register-only loop of dense bf16 32x32x16 MFMAs: `groups` workgroups of 256 threads, each
+ * wave running 8 independent accumulator chains for `iters` iterations, with no memory traffic
+ * except one float per thread written to out[groups * 256] at the end (a caller-owned device
+ * buffer of at least groups * 256 floats; its values mean nothing).  Timing the launch gives the
+ * matrix-core rate the chip sustains at the clock it holds under MFMA load, beside the dense
+ * bf16 peak that the step's matrix-bound kernels are rated against.
+ * eb_probe_mfma_bf16_flops returns the launch's flop count (2 * 32 * 32 * 16 per MFMA), or 0.0
+ * for arguments the probe rejects.  groups in [1, 65536], iters in [1, 2^20], else
+ * EB_ERR_INVALID and nothing is launched.
+ * ------------------------------------------------------------------------------------- */
+eb_status eb_probe_mfma_bf16(float* out, int32_t groups, int32_t iters, eb_stream_t stream);
+double eb_probe_mfma_bf16_flops(int32_t groups, int32_t iters);
+
+/* ---------------------------------------------------------------------------------------
  * Diagnostics.
  * ------------------------------------------------------------------------------------- */
 const char* eb_status_string(eb_status s); /* static string */

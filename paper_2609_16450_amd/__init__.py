@@ -7,7 +7,7 @@ from .binding import (EB_BF16, EB_F32, EbError, Ragged, StepBuffers, eb_block_at
                       eb_block_attn_workspace, eb_decode_step,
                       eb_decode_step_attn_in_lmhead, eb_decode_step_workspace, eb_last_error, eb_lbs_select, eb_lmhead_confidence, eb_lmhead_features,
                       eb_lmhead_features_workspace, eb_lmhead_workspace, eb_lps_features,
-                      eb_status_string, eb_unmask_select, eb_unmask_select_lps,
+                      eb_probe_mfma_bf16, eb_status_string, eb_unmask_select, eb_unmask_select_lps,
                       eb_unmask_select_topm, eb_version, lib_path, load)
 
 __all__ = ["EB_BF16", "EB_F32", "EbError", "Ragged", "StepBuffers", "eb_block_attn",
@@ -15,5 +15,5 @@ __all__ = ["EB_BF16", "EB_F32", "EbError", "Ragged", "StepBuffers", "eb_block_at
            "eb_block_attn_workspace", "eb_decode_step",
            "eb_decode_step_attn_in_lmhead", "eb_decode_step_workspace", "eb_last_error", "eb_lbs_select", "eb_lmhead_confidence", "eb_lmhead_features",
            "eb_lmhead_features_workspace", "eb_lmhead_workspace", "eb_lps_features",
-           "eb_status_string", "eb_unmask_select", "eb_unmask_select_lps",
+           "eb_probe_mfma_bf16", "eb_status_string", "eb_unmask_select", "eb_unmask_select_lps",
            "eb_unmask_select_topm", "eb_version", "lib_path", "load"]

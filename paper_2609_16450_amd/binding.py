@@ -88,6 +88,8 @@ EXPORTS = {
     "eb_decode_step_workspace": (ctypes.c_size_t, [ctypes.POINTER(eb_step_desc)]),
     "eb_decode_step": (ctypes.c_int, [ctypes.POINTER(eb_step_desc), _P, ctypes.c_size_t, _P]),
     "eb_decode_step_attn_in_lmhead": (ctypes.c_int32, [ctypes.POINTER(eb_step_desc)]),
+    "eb_probe_mfma_bf16": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P]),
+    "eb_probe_mfma_bf16_flops": (ctypes.c_double, [ctypes.c_int32, ctypes.c_int32]),
     "eb_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "eb_last_error": (ctypes.c_char_p, []),
     "eb_version": (ctypes.c_char_p, []),
@@ -482,6 +484,18 @@ def eb_decode_step_workspace(buffers: StepBuffers) -> int:
 def eb_decode_step_attn_in_lmhead(buffers: StepBuffers) -> bool:
     """Whether eb_decode_step runs the attention inside the LM-head launch for these buffers."""
     return bool(load().eb_decode_step_attn_in_lmhead(ctypes.byref(buffers.desc)))
+
+
+def eb_probe_mfma_bf16(out: torch.Tensor, groups: int, iters: int, stream=None) -> float:
+    """Launch the register-only bf16 MFMA loop (eb.h, measurement aid) into `out` (float32,
+    at least groups * 256 elements); returns the launch's flop count."""
+    _dev(out, "out", torch.float32)
+    if out.numel() < groups * 256:
+        raise ValueError(f"out holds {out.numel()} floats, the probe writes {groups * 256}")
+    lib = load()
+    _check(lib.eb_probe_mfma_bf16(out.data_ptr(), groups, iters, _stream(stream)),
+           "eb_probe_mfma_bf16")
+    return float(lib.eb_probe_mfma_bf16_flops(groups, iters))
 
 
 def eb_decode_step(buffers: StepBuffers, stream=None, trace: Optional[eb_step_trace] = None) -> None:

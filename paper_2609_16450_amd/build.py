@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libeb.so")
-SOURCES = ["eb_api.hip", "lmhead.hip", "attn.hip", "unmask.hip", "lbs.hip", "step.hip"]
+SOURCES = ["eb_api.hip", "lmhead.hip", "attn.hip", "unmask.hip", "lbs.hip", "step.hip", "probe.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

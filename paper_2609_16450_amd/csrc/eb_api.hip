@@ -41,6 +41,8 @@ eb_status hip_status(hipError_t e, const char* what) {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 constexpr size_t kWsAlign = 256;
+constexpr int kProbeMaxGroups = 65536;
+constexpr int kProbeMaxIters = 1 << 20;
 size_t round_up(size_t n) { return (n + kWsAlign - 1) / kWsAlign * kWsAlign; }
 
 eb_status check_ragged(const eb_ragged* r, bool need_prefix) {
@@ -190,6 +192,20 @@ const char* eb_status_string(eb_status s) {
 const char* eb_last_error(void) { return g_last_error.c_str(); }
 
 const char* eb_version(void) { return "libeb 0.1 (gfx950)"; }
+
+double eb_probe_mfma_bf16_flops(int32_t groups, int32_t iters) {
+  if (groups < 1 || groups > kProbeMaxGroups || iters < 1 || iters > kProbeMaxIters) return 0.0;
+  return eb::mfma_probe_flops(groups, iters);
+}
+
+eb_status eb_probe_mfma_bf16(float* out, int32_t groups, int32_t iters, eb_stream_t stream) {
+  if (!out) return fail(EB_ERR_INVALID, "out is NULL");
+  if (groups < 1 || groups > kProbeMaxGroups)
+    return fail(EB_ERR_INVALID, "groups must be in [1, %d] (got %d)", kProbeMaxGroups, groups);
+  if (iters < 1 || iters > kProbeMaxIters)
+    return fail(EB_ERR_INVALID, "iters must be in [1, %d] (got %d)", kProbeMaxIters, iters);
+  return hip_status(eb::mfma_probe(out, groups, iters, stream), "mfma probe launch");
+}
 
 size_t eb_block_attn_workspace(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim) {
   if (!r || r->batch < 1 || hq < 1 || hkv < 1 || hq % hkv || r->total_block <= 0) return 0;

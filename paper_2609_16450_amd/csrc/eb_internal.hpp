@@ -53,6 +53,12 @@ bool lmhead_hosts_attn(bool bf16, int n_rows, int vocab, const AttnArgs& a);
 hipError_t lmhead_partials_attn(int n_rows, int hidden, int vocab, const void* h, const void* w,
                                 void* ws, const AttnArgs& a, void* attn_ws, hipStream_t s);
 
+// ---- measurement aid -------------------------------------------------------------------
+// Register-only bf16 32x32x16 MFMA loop over `groups` workgroups of 256 threads; each thread
+// writes one float of out[groups * 256].  mfma_probe_flops gives the launch's flop count.
+double mfma_probe_flops(int groups, int iters);
+hipError_t mfma_probe(float* out, int groups, int iters, hipStream_t s);
+
 // ---- unmask ---------------------------------------------------------------------------
 hipError_t unmask_select(int batch, int max_block, const int32_t* cu_block, const float* conf,
                          const int32_t* argmax, const float* tau, uint8_t* masked,

@@ -142,3 +142,16 @@ def test_attention_in_lmhead_query():
     assert q(desc(B.EB_BF16, 1, 16, 16, 4, 4, 128, 262144)) == 0     # 8-wave LM-head launch
     assert q(desc(B.EB_F32, 1, 32, 32, 4, 4, 64, 2048)) == 0          # fp32 path
     assert q(desc(B.EB_BF16, 2, 0, 0, 4, 4, 128, 2048)) == 0          # no block rows
+
+
+def test_mfma_probe_rejects_bad_arguments():
+    lib = B.load()
+    dummy = 0x1000  # never dereferenced: every call below is rejected on the host
+    assert lib.eb_probe_mfma_bf16(None, 1, 1, None) == B.EB_ERR_INVALID
+    assert lib.eb_probe_mfma_bf16(dummy, 0, 1, None) == B.EB_ERR_INVALID
+    assert lib.eb_probe_mfma_bf16(dummy, 65537, 1, None) == B.EB_ERR_INVALID
+    assert lib.eb_probe_mfma_bf16(dummy, 1, 0, None) == B.EB_ERR_INVALID
+    assert lib.eb_probe_mfma_bf16(dummy, 1, (1 << 20) + 1, None) == B.EB_ERR_INVALID
+    assert lib.eb_probe_mfma_bf16_flops(0, 1) == 0.0
+    # 8 chains x 4 waves x 2*32*32*16 flops per MFMA
+    assert lib.eb_probe_mfma_bf16_flops(3, 5) == 3 * 5 * 8 * 4 * 2 * 32 * 32 * 16
