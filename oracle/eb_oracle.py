@@ -203,13 +203,21 @@ def unmask_select(conf, argmax, masked, tokens, tau, cu_block) -> dict:
 # LPS features and the union accept rule
 # --------------------------------------------------------------------------
 
-def lps_features(conf, entropy, top2_gap, masked, cu_block, vocab: int) -> dict:
+def lps_features(conf, entropy, top2_gap, masked, cu_block, vocab: int, seq_pos=None) -> dict:
     """LPS router inputs of every block row (Sec. 5.2, Alg. 5).
 
     feat[i] = (kappa_i, H_i / ln|V|, Delta_i, rho_b) for row i of block b, where rho_b is the
-    fraction of the block's rows still masked before this step's commit; pos[i] = (i - b0) /
-    len_b with b0 the block's first row (rows are packed in ascending sequence position, so
-    i - b0 is the row's rank within the block).  Empty blocks have rho = 0.
+    fraction of the block's rows still masked before this step's commit.  Empty blocks have
+    rho = 0.
+
+    pos[i] is the normalised intra-block position (i - b) / |B| of Sec. 5.2 and Alg. 5, with b
+    the block's left boundary and |B| its size (len_b rows):
+      * seq_pos given (the sequence position of every packed row, ascending within a block):
+        pos[i] = (seq_pos[i] - seq_pos[b0]) / len_b with b0 the block's first row, i.e. the
+        printed formula on sequence positions; for a block with gaps this exceeds 1 towards
+        its right end;
+      * seq_pos None: pos[i] = (i - b0) / len_b, the row's rank within the packed block, which
+        is the printed formula when the block is contiguous and stays in [0, 1) otherwise.
     """
     conf, entropy, top2_gap = _f64(conf), _f64(entropy), _f64(top2_gap)
     T = len(conf)
@@ -224,9 +232,11 @@ def lps_features(conf, entropy, top2_gap, masked, cu_block, vocab: int) -> dict:
         if n == 0:
             continue
         rho[b] = sum(1 for i in range(b0, b1) if masked[i]) / n
+        left = int(seq_pos[b0]) if seq_pos is not None else b0
         for i in range(b0, b1):
             feat[i] = (conf[i], entropy[i] / lnv, top2_gap[i], rho[b])
-            pos[i] = (i - b0) / n
+            where = int(seq_pos[i]) if seq_pos is not None else i
+            pos[i] = (where - left) / n
     return {"feat": feat, "pos": pos, "mask_ratio": rho}
 
 
@@ -309,17 +319,20 @@ def unmask_select_topm(conf, argmax, masked, tokens, tau, cu_block, m: int) -> d
 # --------------------------------------------------------------------------
 
 def lbs_select(masked, p_phi, x_hat, eos_id: int, l_min: int, l_b: int, g_max: int) -> dict:
-    """Active-block selection of Alg. 5 (Sec. 5.1) for each sequence of a batch.
+    """Block selection of the LBS router's post-pass (Sec. 5.1; Alg. 5) for each sequence.
 
-    masked, p_phi, x_hat [n_seq, L] over the generation window.  With M the masked positions of
-    a sequence (ascending):
-      if |M| <= l_min: B = M (size fallback);
-      else C = {i in M : p_phi_i > 0.5 and x_hat_i != eos_id} (router candidates, EOS removal);
-           B = C cut at its first position whose distance to the previous kept position
-               exceeds g_max, that position and every later one dropped (max-gap filter);
-           if |B| < l_min: B = the first l_b positions of M (min-tokens fallback).
-    p_phi is an fp32 input compared with 0.5 exactly.  Returns the block as a 0/1 mask
-    [n_seq, L] (u8), its size and its first position (-1 when empty).
+    Inputs cover the generation window: masked, p_phi (the router's inclusion probability, an
+    fp32 input compared with 0.5 exactly) and x_hat, each [n_seq, L].  For one sequence, with M
+    its masked positions in ascending order:
+      * a sequence with at most l_min masked positions takes all of them as its block;
+      * otherwise the block is grown from the left over the masked positions the router
+        includes (p_phi > 0.5) and whose predicted token is not eos_id; it stops before the
+        first such position lying more than g_max positions after the last one taken, so
+        positions past a wide gap never join;
+      * a block grown this way with fewer than l_min positions is replaced by the l_b lowest
+        positions of M.
+    Returns the block as a 0/1 mask [n_seq, L] (u8), its size and its first position (-1 when
+    empty).
     """
     masked = np.asarray(masked)
     p_phi = np.asarray(p_phi, dtype=np.float32).astype(np.float64)

@@ -118,6 +118,71 @@ def test_lps_features_hand_derived():
     np.testing.assert_allclose(r["feat"][5], [0.6, 0.5 / math.log(4), 0.3, 0.0])
 
 
+def _golden_positions():
+    from fractions import Fraction
+    cases = []
+    for lhs, rhs in _rows("lps_position_examples.txt"):
+        cases.append((lhs[0], _ints(lhs[1]), [Fraction(x) for x in rhs[0].split()]))
+    return cases
+
+
+def test_lps_positions_printed_formula_golden():
+    # all hand-derived blocks as one ragged batch, placed at unrelated packed offsets
+    cases = _golden_positions()
+    lens = [len(c[1]) for c in cases]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    seq_pos = np.concatenate([c[1] for c in cases]).astype(np.int32)
+    T = int(cu[-1])
+    z = np.zeros(T)
+    r = lps_features(z, z, z, np.ones(T, np.uint8), cu, vocab=10, seq_pos=seq_pos)
+    for b, (name, _, want) in enumerate(cases):
+        got = r["pos"][cu[b]:cu[b + 1]]
+        np.testing.assert_allclose(got, [float(x) for x in want], rtol=0, atol=1e-15,
+                                   err_msg=name)
+
+
+def test_lps_positions_contiguous_blocks_equal_rank_form():
+    # a contiguous block's sequence positions differ from its packed rows by a constant, so the
+    # printed formula and the rank form agree there
+    rng = np.random.default_rng(14)
+    lens = [0, 1, 7, 32, 5]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    seq_pos = np.concatenate([np.arange(n) + rng.integers(0, 400) for n in lens]).astype(np.int32)
+    x = rng.random(T)
+    masked = (rng.random(T) < 0.5).astype(np.uint8)
+    a = lps_features(x, x, x, masked, cu, vocab=50, seq_pos=seq_pos)
+    b = lps_features(x, x, x, masked, cu, vocab=50)
+    np.testing.assert_array_equal(a["pos"], b["pos"])
+    np.testing.assert_array_equal(a["feat"], b["feat"])
+
+
+def test_lps_positions_on_lbs_blocks():
+    # blocks chosen by the LBS post-pass with g_max = 5: each position's value is its distance
+    # from the block's first position over the block size, and a block with a gap reaches past 1
+    rng = np.random.default_rng(15)
+    n, L = 6, 64
+    masked = (rng.random((n, L)) < 0.8).astype(np.uint8)
+    p_phi = rng.random((n, L)).astype(np.float32)
+    x_hat = rng.integers(0, 9, (n, L)).astype(np.int32)
+    sel = lbs_select(masked, p_phi, x_hat, eos_id=8, l_min=2, l_b=8, g_max=5)
+    rows = [np.nonzero(sel["block"][s])[0] for s in range(n)]
+    lens = [len(x) for x in rows]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    seq_pos = np.concatenate(rows).astype(np.int32)
+    T = int(cu[-1])
+    z = np.zeros(T)
+    r = lps_features(z, z, z, np.ones(T, np.uint8), cu, vocab=10, seq_pos=seq_pos)
+    some_gap = False
+    for s in range(n):
+        got = r["pos"][cu[s]:cu[s + 1]]
+        if lens[s]:
+            assert got[0] == 0.0
+            np.testing.assert_allclose(got * lens[s], rows[s] - rows[s][0], rtol=0, atol=1e-12)
+            some_gap |= bool((np.diff(rows[s]) > 1).any())
+    assert some_gap and r["pos"].max() > 1.0
+
+
 def test_lps_features_ranges_random():
     rng = np.random.default_rng(13)
     lens = rng.integers(0, 30, 9)

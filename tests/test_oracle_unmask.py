@@ -74,14 +74,18 @@ def test_golden_as_one_ragged_batch():
 
 
 def alg5_block(conf, masked, argmax, tokens, tau):
-    """Alg. 5 for one block, written as scalar steps in float32."""
+    """Alg. 5's accept / fallback / commit for one block, as plain scalar steps.
+
+    conf is compared as given (float32 inputs widen exactly); tau as the exact widening of its
+    float32 value."""
     n = len(conf)
-    tau = np.float32(tau)
-    A = [i for i in range(n) if masked[i] == 1 and np.float32(conf[i]) >= tau]
+    tau = float(np.float32(tau))
+    conf = [float(c) for c in conf]
+    A = [i for i in range(n) if masked[i] == 1 and conf[i] >= tau]
     if len(A) == 0:
         best = -1
         for i in range(n):
-            if masked[i] == 1 and (best < 0 or np.float32(conf[i]) > np.float32(conf[best])):
+            if masked[i] == 1 and (best < 0 or conf[i] > conf[best]):
                 best = i
         A = [best] if best >= 0 else []
     x = list(tokens)
@@ -95,39 +99,57 @@ def alg5_block(conf, masked, argmax, tokens, tau):
 LEVELS = np.array([0.1, 0.5, 0.9, 0.95, 1.0], dtype=np.float32)
 
 
-@pytest.mark.parametrize("n", [1, 2, 3, 4])
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 6])
 def test_exhaustive_small_blocks(n):
+    # every mask pattern of n positions x every confidence vector over LEVELS (exact ties and
+    # kappa == tau included); all confidence vectors of one mask pattern go through the oracle
+    # as one ragged batch of blocks
     tau = np.float32(0.9)
+    confs = np.array(list(itertools.product(LEVELS, repeat=n)), np.float32)
+    C = confs.shape[0]
     argmax = np.arange(100, 100 + n, dtype=np.int32)
+    cu = (np.arange(C + 1) * n).astype(np.int32)
+    conf_rows = [[float(c) for c in row] for row in confs]
     for mask_bits in itertools.product([0, 1], repeat=n):
         masked = np.array(mask_bits, np.uint8)
         tokens = np.where(masked == 1, -1, np.arange(n)).astype(np.int32)
-        for conf in itertools.product(LEVELS, repeat=n):
-            conf = np.array(conf, np.float32)
-            r = unmask_select(conf, argmax, masked, tokens, [tau], np.array([0, n], np.int32))
-            A, x, m, res = alg5_block(conf, masked, argmax, tokens, tau)
-            exp_unmask = np.zeros(n, np.uint8)
-            exp_unmask[A] = 1
-            np.testing.assert_array_equal(r["unmask"], exp_unmask)
-            np.testing.assert_array_equal(r["tokens"], x)
-            np.testing.assert_array_equal(r["masked"], m)
-            assert r["n_commit"][0] == len(A) and r["resolved"][0] == res
+        r = unmask_select(confs.ravel(), np.tile(argmax, C), np.tile(masked, C),
+                          np.tile(tokens, C), np.full(C, tau, np.float32), cu)
+        exp_unmask = np.zeros((C, n), np.uint8)
+        exp_tokens = np.empty((C, n), np.int32)
+        exp_masked = np.empty((C, n), np.uint8)
+        exp_commit = np.empty(C, np.int32)
+        exp_res = np.empty(C, np.uint8)
+        ml, al, tl = list(mask_bits), argmax.tolist(), tokens.tolist()
+        for c in range(C):
+            A, x, m, res = alg5_block(conf_rows[c], ml, al, tl, tau)
+            exp_unmask[c, A] = 1
+            exp_tokens[c] = x
+            exp_masked[c] = m
+            exp_commit[c] = len(A)
+            exp_res[c] = res
+        np.testing.assert_array_equal(r["unmask"].reshape(C, n), exp_unmask)
+        np.testing.assert_array_equal(r["tokens"].reshape(C, n), exp_tokens)
+        np.testing.assert_array_equal(r["masked"].reshape(C, n), exp_masked)
+        np.testing.assert_array_equal(r["n_commit"], exp_commit)
+        np.testing.assert_array_equal(r["resolved"], exp_res)
 
 
 @pytest.mark.parametrize("n", [5, 6])
-def test_sampled_blocks_with_ties(n):
+def test_sampled_blocks_other_tau(n):
+    # tau = 0.5 sits on a level too; sampled, with random argmax ids and unmasked tokens
     rng = np.random.default_rng(n)
-    for tau in (np.float32(0.9), np.float32(0.5)):
-        for _ in range(1500):
-            masked = (rng.random(n) < 0.6).astype(np.uint8)
-            conf = LEVELS[rng.integers(0, LEVELS.size, n)]
-            argmax = rng.integers(0, 50, n).astype(np.int32)
-            tokens = np.where(masked == 1, -1, rng.integers(0, 50, n)).astype(np.int32)
-            r = unmask_select(conf, argmax, masked, tokens, [tau], np.array([0, n], np.int32))
-            A, x, m, res = alg5_block(conf, masked, argmax, tokens, tau)
-            assert sorted(np.nonzero(r["unmask"])[0].tolist()) == sorted(A)
-            np.testing.assert_array_equal(r["tokens"], x)
-            assert r["resolved"][0] == res
+    tau = np.float32(0.5)
+    for _ in range(1500):
+        masked = (rng.random(n) < 0.6).astype(np.uint8)
+        conf = LEVELS[rng.integers(0, LEVELS.size, n)]
+        argmax = rng.integers(0, 50, n).astype(np.int32)
+        tokens = np.where(masked == 1, -1, rng.integers(0, 50, n)).astype(np.int32)
+        r = unmask_select(conf, argmax, masked, tokens, [tau], np.array([0, n], np.int32))
+        A, x, m, res = alg5_block(conf, masked, argmax, tokens, tau)
+        assert sorted(np.nonzero(r["unmask"])[0].tolist()) == sorted(A)
+        np.testing.assert_array_equal(r["tokens"], x)
+        assert r["resolved"][0] == res
 
 
 def test_invariants_random_ragged():
