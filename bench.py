@@ -1,13 +1,18 @@
 """Throughput of one Early-Bird denoising step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--legs A,B]
+                    [--no-cpu-baseline]
+    python bench.py --ingest-counters DIR    (rocprofv3 FETCH_SIZE / WRITE_SIZE runs -> traffic)
 
 A step is eb_decode_step over one batch of synthetic, seeded input already resident in HBM:
 block attention over the cached prefix + block keys, the fused LM head with its
 softmax / entropy / confidence / argmax reduction, and threshold unmasking in every block.
-Prints ONE JSON line: positions/s = block positions / step time, the roofline of the fused
-LM-head kernel (timed with hipEvents recorded by the library around that kernel), and the
-fp64 CPU oracle timed on a bounded sample of the same workload.
+Prints ONE JSON line for the headline workload (default: the Dream-7B-shaped batch-64 step,
+the largest configuration that fits one GPU): positions/s = block positions / step time, the
+roofline of the fused LM-head kernel (timed with hipEvents recorded by the library around that
+kernel), further workloads as nested legs with the same fields (default: the LLaDA-8B-shaped
+batch-1 step, the HBM-bound case), and the fp64 CPU oracle timed on a bounded sample of the
+headline workload.
 """
 from __future__ import annotations
 
@@ -87,10 +92,25 @@ def measured_traffic(workload: str):
     return rec.get("bytes_per_launch")
 
 
+def cpu_model() -> str:
+    """The host CPU's model name from /proc/cpuinfo (platform.processor() gives only the ISA)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 def cpu_baseline(case, budget_s: float = 15.0):
-    """Time the fp64 oracle (as it stands) on a bounded sample of the workload."""
-    import numpy as np
-    from threadpoolctl import threadpool_limits
+    """Time the fp64 oracle (as it stands) on a bounded sample of the workload.
+
+    The oracle's step is block_attention, then lmhead_confidence, then unmask_select (what
+    oracle.decode_step runs); the three are timed one after another so that each stage's time
+    is reported, and their sum is the step time."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     import oracle
     from workloads import bf16_bits_to_f32
@@ -106,20 +126,35 @@ def cpu_baseline(case, budget_s: float = 15.0):
     cu_p = case.cu_prefix[:nb + 1]
     T, S = int(cu_b[-1]), int(cu_p[-1])
     w = f(case.w)
-    args = (f(case.q[:T]), f(case.k_blk[:T]), f(case.v_blk[:T]), f(case.k_pre[:S]),
-            f(case.v_pre[:S]), cu_b, cu_p, case.cfg.hq, case.cfg.hkv, f(case.h[:T]), w,
-            case.masked[:T], case.tokens[:T], case.tau[:nb])
+    q, kb, vb = f(case.q[:T]), f(case.k_blk[:T]), f(case.v_blk[:T])
+    kp, vp, h = f(case.k_pre[:S]), f(case.v_pre[:S]), f(case.h[:T])
+    stage = {"attention": 0.0, "lmhead_and_statistics": 0.0, "unmask": 0.0}
     reps, t_total = 0, 0.0
     with threadpool_limits(limits=threads):
+        blas = [{k: d.get(k) for k in ("internal_api", "version", "num_threads", "threading_layer")}
+                for d in threadpool_info() if d.get("user_api") == "blas"]
         while t_total < budget_s and reps < 50:
             t0 = time.perf_counter()
-            oracle.decode_step(*args)
-            t_total += time.perf_counter() - t0
+            oracle.block_attention(q, kb, vb, kp, vp, cu_b, cu_p, case.cfg.hq, case.cfg.hkv)
+            t1 = time.perf_counter()
+            st = oracle.lmhead_confidence(h, w)
+            t2 = time.perf_counter()
+            oracle.unmask_select(st["conf"], st["argmax"], case.masked[:T], case.tokens[:T],
+                                 case.tau[:nb], cu_b)
+            t3 = time.perf_counter()
+            stage["attention"] += t1 - t0
+            stage["lmhead_and_statistics"] += t2 - t1
+            stage["unmask"] += t3 - t2
+            t_total += t3 - t0
             reps += 1
     return {"value": reps * T / t_total, "unit": "positions/s", "cores": threads, "kind": "oracle",
-            "sample": f"{reps} x oracle decode_step over the first {nb} block(s) ({T} block "
+            "sample": f"{reps} x the oracle's step (block_attention, lmhead_confidence, "
+                      f"unmask_select) over the first {nb} block(s) of the workload ({T} block "
                       f"positions, full vocabulary {case.cfg.vocab}, prefix {S}), fp64 numpy, "
-                      f"{t_total:.1f} s on {platform.processor() or platform.machine()}"}
+                      f"{t_total:.1f} s",
+            "threads": threads, "host_cpu_count": os.cpu_count(), "cpu_model": cpu_model(),
+            "blas": blas,
+            "stage_seconds_per_step": {k: v / reps for k, v in stage.items()}}
 
 
 SUFFIX_LEN = 256         # cached suffix rows per sequence on the dual-cache leg
@@ -299,16 +334,194 @@ def variant_leg(args, torch, eb, case, copies, stream) -> int:
     return 0
 
 
+def roofline_of(cfg, T: int, S: int, kernel_ms: float, with_attn: bool) -> dict:
+    """Roofline object of the fused LM-head launch: algorithmic bytes (W, h, results; plus the
+    attention's Q, K, V and O when that launch also runs it) or flops over its duration, bound
+    chosen by arithmetic intensity against the ridge of the spec peaks."""
+    nbytes, flops = lmhead_work(cfg, T)
+    if with_attn:
+        nbytes += attention_bytes(cfg, T, S)
+    ai = flops / nbytes
+    if cfg.dtype == "f32":
+        bound, peak, unit, achieved = "alu", MFMA_F32_PEAK_TFLOPS, "TFLOP/s", flops / (kernel_ms * 1e-3) / 1e12
+    elif ai < (MFMA_BF16_PEAK_TFLOPS * 1e12) / (HBM_PEAK_GBS * 1e9):
+        bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", nbytes / (kernel_ms * 1e-3) / 1e9
+    else:
+        bound, peak, unit, achieved = "mfma", MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", flops / (kernel_ms * 1e-3) / 1e12
+    return {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+            "frac": achieved / peak, "traffic": measured_traffic(cfg.name),
+            "kernel": lmhead_kernel_name(cfg.dtype, T), "kernel_us": kernel_ms * 1e3,
+            "algorithmic_bytes": nbytes, "includes_attention": bool(with_attn),
+            "algorithmic_flops": flops}
+
+
+def step_leg(torch, eb, name: str, steps: int, warmup: int, n_copies: int, stream) -> tuple:
+    """Time `steps` whole eb_decode_step calls of workload `name` (after `warmup`), then the same
+    steps again with hipEvents recorded by the library around the fused LM-head kernel.
+    Returns (fields of the JSON line, the generated case)."""
+    from paper_2609_16450_amd.binding import eb_step_trace
+    from paper_2609_16450_amd.device_case import DeviceStep
+    from workloads import CONFIGS, make_step
+
+    cfg = CONFIGS[name]
+    log(f"bench: generating {cfg.name}")
+    case = make_step(cfg)
+    T = case.T
+    copies = [DeviceStep(case, device="cuda:0") for _ in range(max(1, n_copies))]
+    log(f"bench: {cfg.name} T={T} S={case.S} warmup={warmup} steps={steps}")
+
+    def run(i, trace=None):
+        ds = copies[i % len(copies)]
+        eb.eb_decode_step(ds.buffers, stream=stream, trace=trace)
+
+    for i in range(warmup):
+        run(i)
+    torch.cuda.synchronize()
+
+    # K whole steps, host clock between two synchronisations (events beside it)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(steps):
+        run(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / steps
+    ms_events = ev0.elapsed_time(ev1) / steps
+    log(f"bench: {cfg.name} {ms_per_step:.4f} ms/step (events {ms_events:.4f})")
+
+    # the same steps again with hipEvents recorded around the fused LM-head kernel, on the
+    # step's stream
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for a, b in evs:            # create the events
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        run(i, eb_step_trace(0, 0, a.cuda_event, b.cuda_event, 0, 0))
+    torch.cuda.synchronize()
+    lm_ms = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+    # in small steps the launch also runs the attention: count its algorithmic bytes as well
+    with_attn = eb.eb_decode_step_attn_in_lmhead(copies[0].buffers)
+    roof = roofline_of(cfg, T, case.S, lm_ms, with_attn)
+    log(f"bench: {cfg.name} fused LM-head kernel {lm_ms * 1e3:.1f} us, "
+        f"{roof['achieved']:.1f} {roof['unit']} ({100 * roof['frac']:.1f}%)")
+    fields = {
+        "value": T / (ms_per_step * 1e-3),
+        "unit": "positions/s",
+        "ms_per_step": ms_per_step,
+        "dtype": cfg.dtype,
+        "config": {"workload": cfg.name, "batch": cfg.batch, "block_positions": T,
+                   "prefix_positions": case.S, "heads": f"{cfg.hq}/{cfg.hkv}x{cfg.head_dim}",
+                   "hidden": cfg.hidden, "vocab": cfg.vocab, "input_copies": len(copies),
+                   "ms_per_step_events": ms_events},
+        "roofline": roof,
+    }
+    del copies
+    torch.cuda.empty_cache()
+    return fields, case
+
+
+def ingest_counters(directory: str) -> int:
+    """Turn rocprofv3 counter runs into profiles/lmhead_traffic.json.
+
+    `directory` holds one rocprofv3 output folder per run, named <run>_FETCH_SIZE and
+    <run>_WRITE_SIZE, each with a *counter_collection.csv: the run "copy" is
+    `bench.py --calibrate-copy 1073741824` (three 1 GiB device-to-device copies); every other
+    run is a bench.py step run whose workloads are listed in the file <run>.workloads (one name
+    per line; a missing file means the run's name is the workload).  Each counter is averaged
+    over the dispatches of the workload's fused LM-head kernel (matched by name), scaled by the
+    factor that makes the copy's reading equal its true bytes (read for FETCH_SIZE, written for
+    WRITE_SIZE), and stored with the hash of the kernel source it was taken on."""
+    import csv
+    import glob
+
+    from workloads import CONFIGS, make_step
+
+    def rows(run, counter):
+        paths = glob.glob(os.path.join(directory, f"{run}_{counter}", "**",
+                                       "*counter_collection.csv"), recursive=True)
+        if not paths:
+            raise SystemExit(f"no counter_collection.csv for {run}_{counter} under {directory}")
+        out = []
+        for p in paths:
+            with open(p, newline="") as f:
+                out += [r for r in csv.DictReader(f) if r["Counter_Name"] == counter]
+        return out
+
+    copy_bytes = 1 << 30
+    factor = {}
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        vals = [float(r["Counter_Value"]) for r in rows("copy", counter)
+                if "copyBuffer" in r["Kernel_Name"]]
+        vals = [v for v in vals if v > 0.25 * copy_bytes / 1024 / 2]   # the 1 GiB copies only
+        if not vals:
+            raise SystemExit(f"no 1 GiB copy dispatch in copy_{counter}")
+        factor[counter] = (copy_bytes / 1024) / (sum(vals) / len(vals))
+    runs = sorted({os.path.basename(d).rsplit("_", 2)[0]
+                   for d in glob.glob(os.path.join(directory, "*_FETCH_SIZE"))} - {"copy"})
+    try:
+        with open(TRAFFIC_FILE) as f:
+            table = json.load(f)
+    except (OSError, ValueError):
+        table = {}
+    src_hash = lmhead_source_hash()
+    for run in runs:
+        wl_file = os.path.join(directory, f"{run}.workloads")
+        names = ([ln.strip() for ln in open(wl_file) if ln.strip()] if os.path.exists(wl_file)
+                 else [run])
+        for name in names:
+            cfg = CONFIGS[name]
+            kernel = lmhead_kernel_name(cfg.dtype, make_step(cfg).T)
+            rec = {"kernel": kernel}
+            total = 0.0
+            for counter, key in (("FETCH_SIZE", "fetch_kib"), ("WRITE_SIZE", "write_kib")):
+                vals = [float(r["Counter_Value"]) for r in rows(run, counter)
+                        if kernel in r["Kernel_Name"]]
+                if not vals:
+                    raise SystemExit(f"{run}_{counter}: no dispatch of {kernel}")
+                rec[key] = sum(vals) / len(vals)
+                rec.setdefault("dispatches", []).append(len(vals))
+                total += rec[key] * 1024 * factor[counter]
+            rec["bytes_per_launch"] = total
+            rec["source_hash"] = src_hash
+            table[name] = rec
+            log(f"ingest: {name} {kernel} {total / 1e9:.4f} GB per launch")
+    table["_note"] = (
+        "HBM-side bytes per launch of the fused LM-head kernel from rocprofv3 FETCH_SIZE and "
+        "WRITE_SIZE (KiB per dispatch, mean over the dispatches of the run), each scaled by what "
+        f"the counter reads for a 1 GiB device-to-device copy: fetch factor "
+        f"{factor['FETCH_SIZE']:.4f}, write factor {factor['WRITE_SIZE']:.4f}. source_hash = "
+        "sha256 of the code of lmhead.hip, eb_common.hpp, attn_small.hpp and attn_common.hpp "
+        "with comments and whitespace removed (first 16 hex digits) when the counters were "
+        "taken. Written by `python bench.py --ingest-counters DIR`; commands in "
+        "profiles/lmhead_counters.md. For a batch-1 step the launch also runs the step's block "
+        "attention (queued behind the vocabulary slices), whose bytes are included.")
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(dict(sorted(table.items())), f, indent=1)
+        f.write("\n")
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llada8b_b1")
+    ap.add_argument("--workload", default="dream7b_b64",
+                    help="headline workload (default: the batch-64 Dream-7B-shaped step)")
+    ap.add_argument("--legs", default="llada8b_b1",
+                    help="comma-separated further workloads timed as nested legs of the same "
+                         "line (default: the batch-1 LLaDA-8B-shaped step; '' for none)")
     ap.add_argument("--copies", type=int, default=2, help="input copies rotated between steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 3 device-to-device copies of BYTES (calibrates HBM counters)")
+    ap.add_argument("--ingest-counters", metavar="DIR",
+                    help="write profiles/lmhead_traffic.json from rocprofv3 counter runs in DIR")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the same-box copy and GEMM reference rates (e.g. under a profiler)")
     ap.add_argument("--path", default="step", choices=["step", "lps", "topm", "dual", "lbs"],
@@ -318,6 +531,8 @@ def main() -> int:
                          "LBS post-pass over a 512-position generation window per sequence")
     args = ap.parse_args()
 
+    if args.ingest_counters:
+        return ingest_counters(args.ingest_counters)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the step is built and timed on a single MI355X "
               "(how the step would shard across GPUs is a design note only).", file=sys.stderr)
@@ -326,7 +541,6 @@ def main() -> int:
     import torch
 
     import paper_2609_16450_amd as eb
-    from paper_2609_16450_amd.binding import eb_step_trace
     from paper_2609_16450_amd.device_case import DeviceStep
     from workloads import CONFIGS, make_step
 
@@ -343,88 +557,39 @@ def main() -> int:
         print(json.dumps({"copy_bytes": args.calibrate_copy, "copies": 3}), flush=True)
         return 0
     eb.load()
-    cfg = CONFIGS[args.workload]
-    log(f"bench: generating {cfg.name}")
-    case = make_step(cfg)
-    T = case.T
-    copies = [DeviceStep(case, device="cuda:0") for _ in range(max(1, args.copies))]
     stream = torch.cuda.current_stream()
-    log(f"bench: T={T} S={case.S} warmup={args.warmup} steps={args.steps}")
 
     if args.path != "step":
+        cfg = CONFIGS[args.workload]
+        log(f"bench: generating {cfg.name}")
+        case = make_step(cfg)
+        copies = [DeviceStep(case, device="cuda:0") for _ in range(max(1, args.copies))]
+        log(f"bench: T={case.T} S={case.S} warmup={args.warmup} steps={args.steps}")
         return variant_leg(args, torch, eb, case, copies, stream)
 
-    def run(i, trace=None):
-        ds = copies[i % len(copies)]
-        eb.eb_decode_step(ds.buffers, stream=stream, trace=trace)
-
-    for i in range(args.warmup):
-        run(i)
-    torch.cuda.synchronize()
-
-    # headline: K whole steps, host clock between two synchronisations
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for i in range(args.steps):
-        run(i)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    ms_events = ev0.elapsed_time(ev1) / args.steps
-    log(f"bench: {ms_per_step:.4f} ms/step (events {ms_events:.4f})")
-
-    # roofline: the same steps again with hipEvents recorded around the fused LM-head kernel
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
-    for a, b in evs:            # create the events
-        a.record(stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    for i, (a, b) in enumerate(evs):
-        run(i, eb_step_trace(0, 0, a.cuda_event, b.cuda_event, 0, 0))
-    torch.cuda.synchronize()
-    lm_ms = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
-    nbytes, flops = lmhead_work(cfg, T)
-    # in small steps the launch also runs the attention: count its algorithmic bytes as well
-    with_attn = eb.eb_decode_step_attn_in_lmhead(copies[0].buffers)
-    if with_attn:
-        nbytes += attention_bytes(cfg, T, case.S)
-    ai = flops / nbytes
-    if cfg.dtype == "f32":
-        bound, peak, unit, achieved = "alu", MFMA_F32_PEAK_TFLOPS, "TFLOP/s", flops / (lm_ms * 1e-3) / 1e12
-    elif ai < (MFMA_BF16_PEAK_TFLOPS * 1e12) / (HBM_PEAK_GBS * 1e9):
-        bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", nbytes / (lm_ms * 1e-3) / 1e9
-    else:
-        bound, peak, unit, achieved = "mfma", MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", flops / (lm_ms * 1e-3) / 1e12
-    log(f"bench: fused LM-head kernel {lm_ms * 1e3:.1f} us, {achieved:.1f} {unit}")
-
+    head, case = step_leg(torch, eb, args.workload, args.steps, args.warmup, args.copies, stream)
+    legs = {}
+    for name in [x.strip() for x in args.legs.split(",") if x.strip() and x.strip() != args.workload]:
+        leg, _ = step_leg(torch, eb, name, args.steps, args.warmup, args.copies, stream)
+        legs[name] = leg
     result = {
         "metric": METRIC,
-        "value": T / (ms_per_step * 1e-3),
-        "unit": "positions/s",
+        "value": head["value"],
+        "unit": head["unit"],
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": cfg.dtype,
+        "dtype": head["dtype"],
         "data": "synthetic",
-        "config": {"workload": cfg.name, "batch": cfg.batch, "block_positions": T,
-                   "prefix_positions": case.S, "heads": f"{cfg.hq}/{cfg.hkv}x{cfg.head_dim}",
-                   "hidden": cfg.hidden, "vocab": cfg.vocab, "input_copies": len(copies),
-                   "ms_per_step_events": ms_events},
-        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": achieved / peak, "traffic": measured_traffic(cfg.name),
-                     "kernel": lmhead_kernel_name(cfg.dtype, T),
-                     "kernel_us": lm_ms * 1e3, "algorithmic_bytes": nbytes,
-                     "includes_attention": with_attn,
-                     "algorithmic_flops": flops},
+        "config": head["config"],
+        "roofline": head["roofline"],
     }
+    if legs:
+        result["legs"] = legs
     if not args.no_peaks:
         result["roofline"]["measured_peak"] = measured_peaks(torch, eb)
         log(f"bench: measured peaks {result['roofline']['measured_peak']}")

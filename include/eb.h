@@ -87,7 +87,8 @@ typedef struct {
  *   q      [T, hq, head_dim]    k_blk, v_blk [T, hkv, head_dim]
  *   k_pre, v_pre [S, hkv, head_dim]             out [T, hq, head_dim]   (all of dtype dt)
  *
- * Requires hq % hkv == 0, head_dim in {64, 128}, scale > 0 (pass 1/sqrt(head_dim)).
+ * Requires hq % hkv == 0, head_dim in {64, 128}, scale > 0 and finite; scale = 0 selects
+ * 1/sqrt(head_dim) (rounded to fp32, the same bits eb_decode_step uses for attn_scale <= 0).
  * Arithmetic: bf16 inputs, fp32 scores / softmax / accumulation, output rounded to bf16
  * (round to nearest even); EB_F32 computes in fp32 throughout.
  * ------------------------------------------------------------------------------------- */
@@ -192,8 +193,20 @@ eb_status eb_lmhead_features(eb_dtype dt, int n_rows, int hidden, int vocab, con
  *
  *   rho_b      = (masked rows of block b) / len_b     (block-wise mask ratio before commit)
  *   feat[i]    = (conf[i], entropy_nats[i] / ln(vocab), top2_gap[i], rho_b)   [T, 4] f32
- *   pos[i]     = (i - cu_block[b]) / len_b            [T] f32 (rank within the packed block)
+ *   pos[i]     = (p_i - p_first) / len_b              [T] f32, the normalised intra-block
+ *                position (i - b) / |B| of Sec. 5.2 and Alg. 5, with b the block's left
+ *                boundary and |B| its size, where
+ *                  seq_pos != NULL:  p_i = seq_pos[i], the sequence position of row i (a
+ *                                    block chosen by eb_lbs_select may have gaps, and then
+ *                                    pos exceeds 1 towards its right end);
+ *                  seq_pos == NULL:  p_i = i, the packed row, so pos is the row's rank within
+ *                                    its block over len_b, in [0, 1) (equal to the above for
+ *                                    a contiguous block);
+ *                p_first is p_i of the block's first row.  Computed in fp32 (the integer
+ *                difference, exact below 2^24, divided by len_b with one rounding).
  *   mask_ratio[b] = rho_b                             [B] f32, optional (NULL to skip)
+ *
+ *   seq_pos [T] i32, optional; ascending within each block (the caller's contract).
  *
  * The router itself is not part of this library: its commit probability p_psi comes back
  * through eb_unmask_select_lps.  Requires vocab >= 2 and feat 16-byte aligned; only r->batch,
@@ -201,8 +214,8 @@ eb_status eb_lmhead_features(eb_dtype dt, int n_rows, int hidden, int vocab, con
  * ------------------------------------------------------------------------------------- */
 eb_status eb_lps_features(const eb_ragged* r, int vocab, const float* conf,
                           const float* entropy_nats, const float* top2_gap,
-                          const uint8_t* masked, float* feat, float* pos, float* mask_ratio,
-                          eb_stream_t stream);
+                          const uint8_t* masked, const int32_t* seq_pos, float* feat, float* pos,
+                          float* mask_ratio, eb_stream_t stream);
 
 /* ---------------------------------------------------------------------------------------
  * Union accept rule of Alg. 5 (Sec. 5.2, LPS router inference): as eb_unmask_select, with
@@ -235,22 +248,23 @@ eb_status eb_unmask_select_topm(const eb_ragged* r, const float* conf, const int
 
 /* ---------------------------------------------------------------------------------------
  * LBS active-block selection post-pass (Sec. 5.1; Alg. 5, block selection) for each of n_seq
- * sequences over a generation window of `window` positions.  With M the masked positions of
- * sequence s (ascending):
+ * sequences over a generation window of `window` positions.
  *
- *   if |M| <= l_min:  B = M                                               (size fallback)
- *   else:  C = { i in M : p_phi[s, i] > 0.5 && x_hat[s, i] != eos_id }   (router, EOS removal)
- *          B = C up to (not including) its first position whose distance to the previous
- *              position of C exceeds g_max                                (max-gap filter)
- *          if |B| < l_min:  B = the first l_b positions of M             (min-tokens fallback)
+ * Contract.  For every sequence s the call picks a set B_s of its masked positions (the next
+ * active block) and writes it as a 0/1 mask.  A sequence with at most l_min masked positions
+ * takes all of them.  Otherwise B_s is grown from the left over the masked positions that the
+ * LBS router includes (p_phi > 0.5, strictly) and whose predicted token is not eos_id, and
+ * growth stops before the first such position that lies more than g_max positions after the
+ * last one taken, so nothing beyond a wide gap joins.  When that leaves fewer than l_min
+ * positions, B_s becomes the l_b lowest masked positions instead.  Distances are differences of
+ * positions: g_max = 1 admits contiguous runs only.
  *
  *   masked [n_seq, window] u8, p_phi [n_seq, window] f32 (the LBS router's probability; the
  *   router itself is not part of this library), x_hat [n_seq, window] i32   (inputs)
- *   block [n_seq, window] u8 (1 = in B), size [n_seq] i32 = |B|,
- *   first [n_seq] i32 = smallest position of B or -1 when B is empty       (outputs)
+ *   block [n_seq, window] u8 (1 = in B_s), size [n_seq] i32 = |B_s|,
+ *   first [n_seq] i32 = smallest position of B_s, or -1 when B_s is empty    (outputs)
  *
- * Distances are differences of positions (g_max = 1 keeps only contiguous runs).  Requires
- * l_min, l_b >= 0 and g_max >= 1.  Integer-exact.
+ * Requires l_min, l_b >= 0 and g_max >= 1.  Integer-exact.
  * ------------------------------------------------------------------------------------- */
 eb_status eb_lbs_select(int32_t n_seq, int32_t window, const uint8_t* masked,
                         const float* p_phi, const int32_t* x_hat, int32_t eos_id, int32_t l_min,

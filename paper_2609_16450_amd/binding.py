@@ -8,7 +8,6 @@ extent of a device allocation.  If libeb.so has not been built, loading raises.
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 from dataclasses import dataclass
 from typing import Optional
@@ -77,7 +76,7 @@ EXPORTS = {
     "eb_lmhead_features": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                           _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "eb_lps_features": (ctypes.c_int, [ctypes.POINTER(eb_ragged), ctypes.c_int, _P, _P, _P, _P,
-                                       _P, _P, _P, _P]),
+                                       _P, _P, _P, _P, _P]),
     "eb_unmask_select_lps": (ctypes.c_int, [ctypes.POINTER(eb_ragged), _P, _P, _P, _P,
                                             ctypes.c_float, _P, _P, _P, _P, _P, _P]),
     "eb_unmask_select_topm": (ctypes.c_int, [ctypes.POINTER(eb_ragged), _P, _P, _P,
@@ -214,11 +213,23 @@ class Ragged:
                          self.max_prefix, self.cu_block.data_ptr(), self.cu_prefix.data_ptr())
 
 
-def _workspace(nbytes: int, ws: Optional[torch.Tensor], device) -> tuple:
+def _torch_stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream))
+
+
+def _workspace(nbytes: int, ws: Optional[torch.Tensor], device, stream) -> tuple:
+    """(pointer, bytes) of the caller's workspace, or of a temporary one.  A temporary is
+    allocated on the stream the kernels run on, so that torch's caching allocator, once the
+    tensor is dropped here, hands its memory only to later work of that same stream."""
     if nbytes == 0:
         return (None if ws is None else ws.data_ptr()), (0 if ws is None else ws.numel())
     if ws is None:
-        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        with torch.cuda.stream(_torch_stream(stream)):
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
     _dev(ws, "ws", torch.uint8)
     return ws.data_ptr(), ws.numel()
 
@@ -244,11 +255,11 @@ def eb_block_attn(r: Ragged, q, k_blk, v_blk, k_pre, v_pre, out, scale: Optional
     _dev(k_pre, "k_pre", q.dtype, (r.total_prefix, hkv, D))
     _dev(v_pre, "v_pre", q.dtype, (r.total_prefix, hkv, D))
     _dev(out, "out", q.dtype, (r.total_block, hq, D))
-    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    scale = 0.0 if scale is None else float(scale)    # 0: the library's 1/sqrt(D)
     rc = r.c()
     lib = load()
     need = int(lib.eb_block_attn_workspace(dt, ctypes.byref(rc), hq, hkv, D))
-    wp, wn = _workspace(need, ws, q.device)
+    wp, wn = _workspace(need, ws, q.device, stream)
     _check(lib.eb_block_attn(dt, ctypes.byref(rc), hq, hkv, D, scale, q.data_ptr(),
                              k_blk.data_ptr(), v_blk.data_ptr(), k_pre.data_ptr(),
                              v_pre.data_ptr(), out.data_ptr(), wp, wn, _stream(stream)),
@@ -272,12 +283,12 @@ def eb_block_attn_dual(r: Ragged, cu_suffix: torch.Tensor, max_suffix: int, q, k
     _dev(v_suf, "v_suf", q.dtype, (U, hkv, D))
     _dev(out, "out", q.dtype, (r.total_block, hq, D))
     _dev(cu_suffix, "cu_suffix", torch.int32, (r.batch + 1,))
-    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    scale = 0.0 if scale is None else float(scale)    # 0: the library's 1/sqrt(D)
     rc = r.c()
     sc = eb_suffix(U, int(max_suffix), cu_suffix.data_ptr())
     lib = load()
     need = int(lib.eb_block_attn_dual_workspace(dt, ctypes.byref(rc), ctypes.byref(sc), hq, hkv, D))
-    wp, wn = _workspace(need, ws, q.device)
+    wp, wn = _workspace(need, ws, q.device, stream)
     _check(lib.eb_block_attn_dual(dt, ctypes.byref(rc), ctypes.byref(sc), hq, hkv, D, scale,
                                   q.data_ptr(), k_blk.data_ptr(), v_blk.data_ptr(),
                                   k_pre.data_ptr(), v_pre.data_ptr(), k_suf.data_ptr(),
@@ -304,7 +315,7 @@ def eb_lmhead_confidence(h, w, conf, entropy_nats, argmax, max_logit=None,
         _dev(max_logit, "max_logit", torch.float32, (n_rows,))
     lib = load()
     need = int(lib.eb_lmhead_workspace(dt, n_rows, hidden, vocab))
-    wp, wn = _workspace(need, ws, h.device)
+    wp, wn = _workspace(need, ws, h.device, stream)
     _check(lib.eb_lmhead_confidence(dt, n_rows, hidden, vocab, h.data_ptr(), w.data_ptr(),
                                     conf.data_ptr(), entropy_nats.data_ptr(), argmax.data_ptr(),
                                     _ptr(max_logit), wp, wn, _stream(stream)),
@@ -350,7 +361,7 @@ def eb_lmhead_features(h, w, conf, entropy_nats, argmax, top2_gap, max_logit=Non
         _dev(max_logit, "max_logit", torch.float32, (n_rows,))
     lib = load()
     need = int(lib.eb_lmhead_features_workspace(dt, n_rows, hidden, vocab))
-    wp, wn = _workspace(need, ws, h.device)
+    wp, wn = _workspace(need, ws, h.device, stream)
     _check(lib.eb_lmhead_features(dt, n_rows, hidden, vocab, h.data_ptr(), w.data_ptr(),
                                   conf.data_ptr(), entropy_nats.data_ptr(), argmax.data_ptr(),
                                   _ptr(max_logit), top2_gap.data_ptr(), wp, wn, _stream(stream)),
@@ -358,20 +369,24 @@ def eb_lmhead_features(h, w, conf, entropy_nats, argmax, top2_gap, max_logit=Non
 
 
 def eb_lps_features(r: Ragged, vocab: int, conf, entropy_nats, top2_gap, masked, feat, pos,
-                    mask_ratio=None, stream=None) -> None:
-    """LPS router inputs feat [T, 4] and intra-block positions pos [T] (eb.h)."""
+                    mask_ratio=None, seq_pos=None, stream=None) -> None:
+    """LPS router inputs feat [T, 4] and intra-block positions pos [T] (eb.h); with seq_pos
+    [T] int32 (sequence position of every packed row) pos is (i - b) / |B| on sequence
+    positions, without it the row's rank in its block over the block size."""
     T, B = r.total_block, r.batch
     for name, t in (("conf", conf), ("entropy_nats", entropy_nats), ("top2_gap", top2_gap),
                     ("pos", pos)):
         _dev(t, name, torch.float32, (T,))
     _dev(masked, "masked", torch.uint8, (T,))
+    if seq_pos is not None:
+        _dev(seq_pos, "seq_pos", torch.int32, (T,))
     _dev(feat, "feat", torch.float32, (T, 4))
     if mask_ratio is not None:
         _dev(mask_ratio, "mask_ratio", torch.float32, (B,))
     rc = r.c()
     _check(load().eb_lps_features(ctypes.byref(rc), int(vocab), conf.data_ptr(),
                                   entropy_nats.data_ptr(), top2_gap.data_ptr(), masked.data_ptr(),
-                                  feat.data_ptr(), pos.data_ptr(), _ptr(mask_ratio),
+                                  _ptr(seq_pos), feat.data_ptr(), pos.data_ptr(), _ptr(mask_ratio),
                                   _stream(stream)),
            "eb_lps_features")
 

@@ -63,6 +63,12 @@ eb_status check_ragged(const eb_ragged* r, bool need_prefix) {
   return EB_OK;
 }
 
+// The attention scale: 0 selects 1 / sqrt(head_dim), computed here in fp32 for every entry point
+// (so that eb_block_attn and eb_decode_step use the same bits).
+float attn_scale_or_default(float scale, int head_dim) {
+  return scale == 0.f && head_dim > 0 ? 1.0f / sqrtf(static_cast<float>(head_dim)) : scale;
+}
+
 eb_status check_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim, float scale,
                      const void* q, const void* k_blk, const void* v_blk, const void* k_pre,
                      const void* v_pre, const void* out) {
@@ -218,6 +224,7 @@ eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int he
                         float scale, const void* q, const void* k_blk, const void* v_blk,
                         const void* k_pre, const void* v_pre, void* out, void* ws,
                         size_t ws_bytes, eb_stream_t stream) {
+  scale = attn_scale_or_default(scale, head_dim);
   eb_status st = check_attn(dt, r, hq, hkv, head_dim, scale, q, k_blk, v_blk, k_pre, v_pre, out);
   if (st != EB_OK) return st;
   const size_t need = eb_block_attn_workspace(dt, r, hq, hkv, head_dim);
@@ -247,6 +254,7 @@ eb_status eb_block_attn_dual(eb_dtype dt, const eb_ragged* r, const eb_suffix* s
                              const void* v_blk, const void* k_pre, const void* v_pre,
                              const void* k_suf, const void* v_suf, void* out, void* ws,
                              size_t ws_bytes, eb_stream_t stream) {
+  scale = attn_scale_or_default(scale, head_dim);
   eb_status st = check_attn(dt, r, hq, hkv, head_dim, scale, q, k_blk, v_blk, k_pre, v_pre, out);
   if (st != EB_OK) return st;
   if (!sfx) return fail(EB_ERR_INVALID, "suffix descriptor is NULL");
@@ -324,8 +332,8 @@ eb_status eb_lmhead_features(eb_dtype dt, int n_rows, int hidden, int vocab, con
 
 eb_status eb_lps_features(const eb_ragged* r, int vocab, const float* conf,
                           const float* entropy_nats, const float* top2_gap,
-                          const uint8_t* masked, float* feat, float* pos, float* mask_ratio,
-                          eb_stream_t stream) {
+                          const uint8_t* masked, const int32_t* seq_pos, float* feat, float* pos,
+                          float* mask_ratio, eb_stream_t stream) {
   eb_status st = check_ragged(r, false);
   if (st != EB_OK) return st;
   if (vocab < 2) return fail(EB_ERR_INVALID, "vocab must be >= 2 (got %d)", vocab);
@@ -336,7 +344,7 @@ eb_status eb_lps_features(const eb_ragged* r, int vocab, const float* conf,
   st = check_device(r, false, nullptr, stream);
   if (st != EB_OK) return st;
   return hip_status(eb::lps_features(r->batch, r->cu_block, vocab, conf, entropy_nats, top2_gap,
-                                     masked, feat, pos, mask_ratio, stream),
+                                     masked, seq_pos, feat, pos, mask_ratio, stream),
                     "eb_lps_features launch");
 }
 
@@ -422,7 +430,7 @@ size_t eb_decode_step_workspace(const eb_step_desc* d) {
 
 eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_stream_t stream) {
   if (!d) return fail(EB_ERR_INVALID, "step descriptor is NULL");
-  const float scale = d->attn_scale > 0.f ? d->attn_scale : 1.0f / sqrtf((float)d->head_dim);
+  const float scale = attn_scale_or_default(d->attn_scale > 0.f ? d->attn_scale : 0.f, d->head_dim);
   eb_status st = check_attn(d->dtype, &d->ragged, d->hq, d->hkv, d->head_dim, scale, d->q,
                             d->k_blk, d->v_blk, d->k_pre, d->v_pre, d->attn_out);
   if (st != EB_OK) return st;

@@ -74,7 +74,8 @@ hipError_t unmask_select_topm(int batch, const int32_t* cu_block, const float* c
                               uint8_t* resolved, hipStream_t s);
 hipError_t lps_features(int batch, const int32_t* cu_block, int vocab, const float* conf,
                         const float* entropy, const float* gap, const uint8_t* masked,
-                        float* feat, float* pos, float* mask_ratio, hipStream_t s);
+                        const int32_t* seq_pos, float* feat, float* pos, float* mask_ratio,
+                        hipStream_t s);
 
 // ---- fused step epilogue ---------------------------------------------------------------
 // One launch after block_attn(..., defer_merge = true) and lmhead_partials: merges the attention

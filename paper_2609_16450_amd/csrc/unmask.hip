@@ -20,13 +20,14 @@ __global__ __launch_bounds__(kThreads) void unmask_kernel(
 }
 
 // LPS router inputs (Sec. 5.2, Alg. 5), one workgroup per block: the block's mask ratio rho
-// before this step's commit, then per row feat = (kappa, H * inv_ln_v, Delta, rho) and
-// pos = (i - b0) / len.
+// before this step's commit, then per row feat = (kappa, H * inv_ln_v, Delta, rho) and the
+// intra-block position pos = (p_i - p_first) / len, where p is the row's sequence position
+// (seq_pos) or, without seq_pos, its packed row index.
 __global__ __launch_bounds__(kThreads) void lps_features_kernel(
     const int32_t* __restrict__ cu_block, float inv_ln_v, const float* __restrict__ conf,
     const float* __restrict__ entropy, const float* __restrict__ gap,
-    const uint8_t* __restrict__ masked, float* __restrict__ feat, float* __restrict__ pos,
-    float* __restrict__ mask_ratio) {
+    const uint8_t* __restrict__ masked, const int32_t* __restrict__ seq_pos,
+    float* __restrict__ feat, float* __restrict__ pos, float* __restrict__ mask_ratio) {
   __shared__ int s_cnt[kThreads / 64];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int beg = cu_block[b], end = cu_block[b + 1], len = end - beg;
@@ -39,10 +40,12 @@ __global__ __launch_bounds__(kThreads) void lps_features_kernel(
   for (int k = 0; k < kThreads / 64; ++k) cnt += s_cnt[k];
   const float rho = len > 0 ? static_cast<float>(cnt) / static_cast<float>(len) : 0.f;
   if (tid == 0 && mask_ratio) mask_ratio[b] = rho;
+  const int first = (seq_pos && len > 0) ? seq_pos[beg] : beg;
   for (int i = beg + tid; i < end; i += kThreads) {
     *reinterpret_cast<f32x4*>(feat + 4 * static_cast<size_t>(i)) =
         f32x4{conf[i], entropy[i] * inv_ln_v, gap[i], rho};
-    pos[i] = static_cast<float>(i - beg) / static_cast<float>(len);
+    const int p = seq_pos ? seq_pos[i] : i;
+    pos[i] = static_cast<float>(p - first) / static_cast<float>(len);
   }
 }
 
@@ -81,10 +84,11 @@ hipError_t unmask_select_topm(int batch, const int32_t* cu_block, const float* c
 
 hipError_t lps_features(int batch, const int32_t* cu_block, int vocab, const float* conf,
                         const float* entropy, const float* gap, const uint8_t* masked,
-                        float* feat, float* pos, float* mask_ratio, hipStream_t s) {
+                        const int32_t* seq_pos, float* feat, float* pos, float* mask_ratio,
+                        hipStream_t s) {
   const float inv_ln_v = static_cast<float>(1.0 / log(static_cast<double>(vocab)));
   hipLaunchKernelGGL(lps_features_kernel, dim3(batch), dim3(kThreads), 0, s, cu_block, inv_ln_v,
-                     conf, entropy, gap, masked, feat, pos, mask_ratio);
+                     conf, entropy, gap, masked, seq_pos, feat, pos, mask_ratio);
   return hipGetLastError();
 }
 

@@ -52,9 +52,11 @@ def test_invalid_arguments_are_rejected_before_launch():
     # misaligned bf16 pointer
     assert lib.eb_block_attn(B.EB_BF16, ctypes.byref(r), 4, 4, 128, 0.1, 0x101, *([0x100] * 5),
                              None, 0, None) == B.EB_ERR_INVALID
-    # non-positive scale
-    assert lib.eb_block_attn(B.EB_BF16, ctypes.byref(r), 4, 4, 128, 0.0, *([0x100] * 6), None, 0,
+    # negative or non-finite scale (0 selects 1/sqrt(head_dim))
+    assert lib.eb_block_attn(B.EB_BF16, ctypes.byref(r), 4, 4, 128, -0.5, *([0x100] * 6), None, 0,
                              None) == B.EB_ERR_INVALID
+    assert lib.eb_block_attn(B.EB_BF16, ctypes.byref(r), 4, 4, 128, float("inf"), *([0x100] * 6),
+                             None, 0, None) == B.EB_ERR_INVALID
     # unknown dtype
     assert lib.eb_lmhead_confidence(7, 4, 64, 100, *([0x100] * 5), None, None, 0, None) == \
         B.EB_ERR_INVALID
@@ -83,8 +85,9 @@ def test_next_row_entry_points_reject_bad_arguments():
     assert lib.eb_lmhead_features(B.EB_BF16, 4, 64, 1000, *([0x100] * 5), None, 0x100, 0x100,
                                   need - 1, None) == B.EB_ERR_WORKSPACE
     # vocab must allow ln(vocab) > 0; feat must be 16-byte aligned
-    assert lib.eb_lps_features(ctypes.byref(r), 1, *([0x100] * 6), None, None) == B.EB_ERR_INVALID
-    assert lib.eb_lps_features(ctypes.byref(r), 100, *([0x100] * 4), 0x104, 0x100, None,
+    assert lib.eb_lps_features(ctypes.byref(r), 1, *([0x100] * 4), None, 0x100, 0x100, None,
+                               None) == B.EB_ERR_INVALID
+    assert lib.eb_lps_features(ctypes.byref(r), 100, *([0x100] * 4), 0x100, 0x104, 0x100, None,
                                None) == B.EB_ERR_INVALID
     # router score required; budget must not be negative
     assert lib.eb_unmask_select_lps(ctypes.byref(r), 0x100, 0x100, 0x100, None, 0.9,

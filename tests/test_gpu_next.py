@@ -372,3 +372,46 @@ def test_lbs_generation_window(window):
     masked, p_phi, x_hat = lbs_window(2024, 64, window, 126464, 126081)
     for l_min, l_b, g_max in ((4, 32, 5), (16, 32, 1), (200, 32, 3)):
         _lbs_compare(masked, p_phi, x_hat, 126081, l_min, l_b, g_max)
+
+
+def test_lps_positions_on_lbs_blocks():
+    # Blocks chosen by eb_lbs_select with g_max = 5 (so some have gaps), gathered in ascending
+    # sequence position as the block rows of a ragged batch; eb_lps_features with the rows'
+    # sequence positions gives Alg. 5's (i - b) / |B|, checked against the oracle, and without
+    # them the rank form.
+    say("lps positions on eb_lbs_select blocks")
+    n, L, V, eos = 32, 512, 152064, 152063
+    masked_w, p_phi, x_hat = lbs_window(2025, n, L, V, eos)
+    sel = _lbs_gpu(masked_w, p_phi, x_hat, eos, 4, 32, 5)
+    ref_sel = oracle.lbs_select(masked_w, p_phi, x_hat, eos, 4, 32, 5)
+    np.testing.assert_array_equal(sel["block"], ref_sel["block"])
+    rows = [np.nonzero(sel["block"][s])[0] for s in range(n)]
+    lens = [len(x) for x in rows]
+    assert any((np.diff(x) > 1).any() for x in rows if len(x) > 1), "no block with a gap"
+    seq_pos = np.concatenate(rows).astype(np.int32)
+    T = int(seq_pos.size)
+    r = Ragged.from_lengths(lens, [0] * n)
+    rng = np.random.default_rng(24)
+    conf = rng.random(T).astype(np.float32)
+    ent = (rng.random(T) * 9).astype(np.float32)
+    gap = (rng.random(T) * conf).astype(np.float32)
+    masked = (rng.random(T) < 0.6).astype(np.uint8)
+    d = lambda x: torch.from_numpy(x).cuda()
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    for with_pos in (True, False):
+        feat = torch.full((T, 4), -7.0, device="cuda")
+        pos = torch.full((T,), -7.0, device="cuda")
+        rho = torch.full((n,), -7.0, device="cuda")
+        eb_lps_features(r, V, d(conf), d(ent), d(gap), d(masked), feat, pos, rho,
+                        seq_pos=d(seq_pos) if with_pos else None)
+        torch.cuda.synchronize()
+        ref = oracle.lps_features(conf, ent, gap, masked, cu, V,
+                                  seq_pos=seq_pos if with_pos else None)
+        got = pos.cpu().numpy()
+        np.testing.assert_allclose(got, ref["pos"], rtol=1e-6, atol=0)
+        np.testing.assert_allclose(feat.cpu().numpy(), ref["feat"], rtol=1e-6, atol=1e-6)
+        np.testing.assert_allclose(rho.cpu().numpy(), ref["mask_ratio"], rtol=0, atol=1e-6)
+        if with_pos:
+            assert got.max() > 1.0
+        else:
+            assert got.max() < 1.0

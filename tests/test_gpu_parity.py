@@ -229,14 +229,23 @@ def test_unmask_random_ragged_with_ties():
 # ----------------------------------------------------------------------------------------
 # whole step on the named workloads, in the launch configuration the benchmark times
 # ----------------------------------------------------------------------------------------
+POSITION_TILE = 256   # block positions per position tile of the large-batch LM-head kernel
+
+
 def _sample_blocks(case, k=3):
+    """Blocks checked element by element on a large workload: the first and the longest block,
+    the last non-empty one (its rows fall in the last, partial position tile), every block with
+    a row among the first 256 block positions (so that one whole position tile is checked row by
+    row), and random ones up to k beyond those."""
     lens = case.block_lens
     nonempty = np.flatnonzero(lens > 0)
     if nonempty.size <= k:
         return nonempty.tolist()
     rng = np.random.default_rng(case.cfg.seed + 77)
-    pick = {int(nonempty[0]), int(nonempty[np.argmax(lens[nonempty])])}
-    while len(pick) < k:
+    pick = {int(nonempty[0]), int(nonempty[np.argmax(lens[nonempty])]), int(nonempty[-1])}
+    pick |= {int(b) for b in nonempty if case.cu_block[b] < POSITION_TILE}
+    want = len(pick) + 1
+    while len(pick) < max(k, want):
         pick.add(int(rng.choice(nonempty)))
     return sorted(pick)
 
@@ -255,6 +264,9 @@ def test_decode_step_workload(name):
     say(f"  gpu done; oracle over blocks {blocks}")
 
     rows = np.concatenate([np.arange(case.cu_block[b], case.cu_block[b + 1]) for b in blocks])
+    if not full:
+        assert set(range(min(POSITION_TILE, case.T))) <= set(rows.tolist())
+        assert case.T - 1 in set(rows.tolist())
     conf = ds.conf.cpu().numpy()
     ent = ds.entropy.cpu().numpy()
     am = ds.argmax.cpu().numpy()
