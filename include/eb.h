@@ -334,6 +334,26 @@ typedef struct {
 size_t eb_decode_step_workspace(const eb_step_desc* d);
 eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_stream_t stream);
 
+/* ---------------------------------------------------------------------------------------
+ * eb_decode_step without a caller workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ *
+ * Same descriptor, same work and bit-identical outputs as eb_decode_step; the workspace is a
+ * device array inside the library of EB_NOALLOC_SCRATCH_BYTES (128 MiB), one per device,
+ * present from the moment the library is loaded on that device until the process ends.  The
+ * call allocates and frees nothing.  On its first call for a device it looks up that device's
+ * copy of the array (the device of `stream`, or the current device for a NULL stream).
+ *
+ * Limit: a step needing more than EB_NOALLOC_SCRATCH_BYTES of workspace
+ * (eb_decode_step_workspace) returns EB_ERR_WORKSPACE and launches nothing.  The array's
+ * contents are left over from the previous call and are not needed to be zero.
+ * Every call on a device shares that device's array: calls that may overlap in time on one
+ * device (different streams without ordering between them, or different threads) race on it
+ * and must be serialised by the caller.
+ * ------------------------------------------------------------------------------------- */
+#define EB_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+eb_status eb_decode_step_noalloc(const eb_step_desc* d, eb_stream_t stream);
+
 /* 1 when eb_decode_step with this descriptor runs the attention's workgroups inside the LM-head
  * launch (the small-step case above), else 0 (also for a NULL descriptor).  Reads only the
  * descriptor's host fields (dtype, ragged sizes, heads, head_dim, vocab); launches nothing.  For

@@ -86,6 +86,7 @@ EXPORTS = {
                                      _P]),
     "eb_decode_step_workspace": (ctypes.c_size_t, [ctypes.POINTER(eb_step_desc)]),
     "eb_decode_step": (ctypes.c_int, [ctypes.POINTER(eb_step_desc), _P, ctypes.c_size_t, _P]),
+    "eb_decode_step_noalloc": (ctypes.c_int, [ctypes.POINTER(eb_step_desc), _P]),
     "eb_decode_step_attn_in_lmhead": (ctypes.c_int32, [ctypes.POINTER(eb_step_desc)]),
     "eb_probe_mfma_bf16": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P]),
     "eb_probe_mfma_bf16_flops": (ctypes.c_double, [ctypes.c_int32, ctypes.c_int32]),
@@ -520,3 +521,15 @@ def eb_decode_step(buffers: StepBuffers, stream=None, trace: Optional[eb_step_tr
     _check(load().eb_decode_step(ctypes.byref(buffers.desc), _ptr(buffers.ws), buffers.ws_bytes,
                                  _stream(stream)),
            "eb_decode_step")
+
+
+EB_NOALLOC_SCRATCH_BYTES = 128 << 20   # the library's per-device scratch (eb.h)
+
+
+def eb_decode_step_noalloc(buffers: StepBuffers, stream=None,
+                           trace: Optional[eb_step_trace] = None) -> None:
+    """The same step with the library's own per-device scratch instead of buffers.ws (eb.h):
+    no device memory is allocated by the call; calls on one device must not overlap."""
+    buffers.desc.trace = ctypes.pointer(trace) if trace is not None else None
+    _check(load().eb_decode_step_noalloc(ctypes.byref(buffers.desc), _stream(stream)),
+           "eb_decode_step_noalloc")

@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -178,6 +179,46 @@ eb_status check_device(const eb_ragged* r, bool need_prefix, const float* tau, h
     st = check_cu("cu_prefix", r->cu_prefix, r->batch, r->total_prefix, r->max_prefix, s);
   if (st == EB_OK && tau) st = check_tau(tau, r->batch, s);
   return st;
+}
+
+// ---------------------------------------------------------------------------------------
+// Device scratch of eb_decode_step_noalloc.  The array exists once per device the library's
+// code object is loaded on and lives until the process ends.  Host code never uses its name
+// as an address (on the host it is only a stand-in for the symbol): the device address of each
+// device's copy comes from hipGetSymbolAddress, taken once per device with that device current,
+// and only that address is passed to kernels.
+// ---------------------------------------------------------------------------------------
+constexpr size_t kNoAllocScratchBytes = EB_NOALLOC_SCRATCH_BYTES;
+static_assert(kNoAllocScratchBytes % 256 == 0, "scratch size is a multiple of the alignment");
+
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+std::vector<void*> g_scratch_addr;  // indexed by device ordinal; nullptr until looked up
+
+// Device address of `scratch` on device `dev` (looked up on the first call for that device).
+eb_status scratch_address(int dev, void** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (dev < 0) return fail(EB_ERR_INVALID, "bad device ordinal %d", dev);
+  if (static_cast<size_t>(dev) >= g_scratch_addr.size()) g_scratch_addr.resize(dev + 1, nullptr);
+  if (!g_scratch_addr[dev]) {
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    void* p = nullptr;
+    if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    const hipError_t e2 = (cur >= 0 && cur != dev) ? hipSetDevice(cur) : hipSuccess;
+    if (e != hipSuccess) return hip_status(e, "scratch symbol lookup");
+    if (e2 != hipSuccess) return hip_status(e2, "restoring the current device");
+    if (!p) return fail(EB_ERR_HIP, "scratch symbol lookup returned NULL");
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return EB_OK;
 }
 
 }  // namespace
@@ -495,6 +536,24 @@ eb_status eb_decode_step(const eb_step_desc* d, void* ws, size_t ws_bytes, eb_st
   }
   if (e == hipSuccess && tr) e = mark(tr->select_end);
   return hip_status(e, "step select launch");
+}
+
+eb_status eb_decode_step_noalloc(const eb_step_desc* d, eb_stream_t stream) {
+  if (!d) return fail(EB_ERR_INVALID, "step descriptor is NULL");
+  const size_t need = eb_decode_step_workspace(d);
+  if (need > kNoAllocScratchBytes)
+    return fail(EB_ERR_WORKSPACE,
+                "step needs %zu bytes of scratch; eb_decode_step_noalloc holds %zu (use "
+                "eb_decode_step with a caller workspace)",
+                need, kNoAllocScratchBytes);
+  int dev = -1;
+  hipError_t e = stream ? hipStreamGetDevice(reinterpret_cast<hipStream_t>(stream), &dev)
+                        : hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "device of the stream");
+  void* ws = nullptr;
+  const eb_status st = scratch_address(dev, &ws);
+  if (st != EB_OK) return st;
+  return eb_decode_step(d, ws, kNoAllocScratchBytes, stream);
 }
 
 }  // extern "C"

@@ -158,3 +158,18 @@ def test_mfma_probe_rejects_bad_arguments():
     assert lib.eb_probe_mfma_bf16_flops(0, 1) == 0.0
     # 8 chains x 4 waves x 2*32*32*16 flops per MFMA
     assert lib.eb_probe_mfma_bf16_flops(3, 5) == 3 * 5 * 8 * 4 * 2 * 32 * 32 * 16
+
+
+def test_noalloc_step_rejects_oversized_steps_on_the_host():
+    # eb_decode_step_noalloc: a step whose workspace exceeds the library's scratch is refused
+    # before anything touches the device
+    lib = B.load()
+    assert lib.eb_decode_step_noalloc(None, None) == B.EB_ERR_INVALID
+    d = B.eb_step_desc()
+    d.dtype = B.EB_BF16
+    d.ragged = B.eb_ragged(64, 20000, 400, 64 * 4096, 4096, 0x1000, 0x2000)
+    d.hq, d.hkv, d.head_dim, d.hidden, d.vocab = 28, 4, 128, 3584, 152064
+    need = lib.eb_decode_step_workspace(ctypes.byref(d))
+    assert need > B.EB_NOALLOC_SCRATCH_BYTES
+    assert lib.eb_decode_step_noalloc(ctypes.byref(d), None) == B.EB_ERR_WORKSPACE
+    assert "scratch" in B.eb_last_error()
