@@ -567,11 +567,13 @@ def main() -> int:
         log(f"bench: T={case.T} S={case.S} warmup={args.warmup} steps={args.steps}")
         return variant_leg(args, torch, eb, case, copies, stream)
 
-    head, case = step_leg(torch, eb, args.workload, args.steps, args.warmup, args.copies, stream)
+    # the legs run first, each with its inputs freshly allocated and freed afterwards, then the
+    # headline workload
     legs = {}
     for name in [x.strip() for x in args.legs.split(",") if x.strip() and x.strip() != args.workload]:
         leg, _ = step_leg(torch, eb, name, args.steps, args.warmup, args.copies, stream)
         legs[name] = leg
+    head, case = step_leg(torch, eb, args.workload, args.steps, args.warmup, args.copies, stream)
     result = {
         "metric": METRIC,
         "value": head["value"],
