@@ -44,6 +44,13 @@ def build_library(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
     if verbose and msgs:
         print("\n".join(msgs))
+    # a library with unresolved symbols (e.g. a kernel whose host-side launch stub the compiler
+    # dropped) links, but cannot be loaded: catch that here rather than at first use
+    import ctypes
+    try:
+        ctypes.CDLL(tmp)
+    except OSError as e:
+        raise RuntimeError(f"built library does not load: {e}") from None
     os.replace(tmp, LIB)
     return LIB
 

@@ -373,30 +373,23 @@ hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, 
 // ---------------------------------------------------------------------------------------
 constexpr int kXcds = 8;
 constexpr int kBand = 4;
-constexpr int kTileBM = 256;
-constexpr int kTileBK = 32;
+constexpr int kTileBM = 256;     // vocabulary rows per tile
+constexpr int kTileBN = 256;     // block positions per tile
+constexpr int kTileBK = 32;      // hidden columns per ring stage
+constexpr int kTileRing = 4;     // ring stages
+constexpr int kTileGroups = 256; // persistent workgroups (one per compute unit)
+constexpr int kBufferWord3 = 0x00020000;  // buffer resource word 3 for raw dword loads on gfx9
 
-struct TileMap {
-  int n_vtiles, n_rtiles, n_bands, grid;
-};
-
-TileMap tile_map(int n_rows, int vocab, int bn) {
-  TileMap m;
-  m.n_vtiles = (vocab + kTileBM - 1) / kTileBM;
-  m.n_rtiles = (n_rows + bn - 1) / bn;
-  m.n_bands = (m.n_vtiles + kBand - 1) / kBand;
-  const int bands_per_xcd = (m.n_bands + kXcds - 1) / kXcds;
-  m.grid = kXcds * bands_per_xcd * kBand * m.n_rtiles;
-  return m;
-}
+int tile_vtiles(int vocab) { return (vocab + kTileBM - 1) / kTileBM; }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void global_void_t;
 
-__device__ __forceinline__ void load_to_lds(const void* g, void* l) {
-  // address-space casts (generic -> global / LDS) need C-style casts
-  __builtin_amdgcn_global_load_lds((global_void_t*)(const_cast<void*>(g)), (lds_void_t*)(l), 16, 0,
-                                   0);
+// 16 bytes per lane from buffer rs at byte offset voff + soff into LDS at l + 16 * lane (a
+// buffer load straight into LDS; the LDS address is wave-uniform).  The builtin sits in a
+// device function of its own: inside a kernel body the host compilation would drop the kernel.
+__device__ __forceinline__ void buffer_load_to_lds(__amdgpu_buffer_rsrc_t rs, void* l,
+                                                   uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(l), 16, voff, soff, 0, 0);
 }
 
 // Partial statistics of one lane's column over TM 32-row MFMA blocks.  Element (tm, r) of the
@@ -476,19 +469,41 @@ __device__ __forceinline__ void wait_vm_lds_and_barrier() {
   asm volatile("s_barrier" ::: "memory");
 }
 
-// 256 x 256 tiles computed by 4 waves as a 2 x 2 grid of 128 x 128 sub-tiles (4 x 4 blocks of
-// 32x32x16 MFMAs, 256 accumulator registers per lane).  Per 32-column k step a wave reads
-// 16 KB of operand fragments from LDS (the 8-wave 128 x 64 split reads 12 KB per wave, 96 KB
-// per tile against 64 KB here).  The fragments of the two 16-column halves of a k step are
-// double-buffered in registers: the reads of one half are issued before the MFMAs of the
-// other, so LDS latency hides under 16 MFMAs.  The DMA ring keeps RING stages occupied: right
-// after the barrier that ends the reads of stage kt, stage kt + RING is issued into its slot.
-template <int RING, bool kTop2>
-__global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
+// Tile (vt, rt) of position s of the launch sequence: bands of kBand vocabulary tiles (the last
+// band may be narrower), each band swept position tile by position tile (vocabulary tiles of the
+// band innermost).  Every s in [0, n_vtiles * n_rtiles) is a tile.
+__device__ __forceinline__ void band_tile(int s, int n_vtiles, int n_rtiles, int& vt, int& rt) {
+  const int per_band = kBand * n_rtiles;
+  const int band = s / per_band;
+  const int tt = s - band * per_band;
+  const int nv = min(kBand, n_vtiles - band * kBand);
+  vt = band * kBand + tt % nv;
+  rt = tt / nv;
+}
+
+// Persistent form of the large-batch kernel: kTileGroups workgroups, one per compute unit, each
+// computing a sequence of 256 x 256 tiles (vocabulary rows x block positions).  The launch
+// sequence is cut into 8 contiguous segments, one per XCD (workgroup g runs on XCD g % 8 and
+// takes every 32nd tile of its XCD's segment), so each XCD gets the same number of tiles and
+// its 32 resident workgroups share a few W and h tiles in its L2.  With fewer tiles than
+// workgroups, workgroup g computes tile g.
+//
+// Per tile: 4 waves form a 2 x 2 grid of 128 x 128 sub-tiles (4 x 4 blocks of 32x32x16 MFMAs,
+// 256 accumulator registers per lane).  Per 32-column k step a wave reads 16 KB of operand
+// fragments from LDS; the fragments of the two 16-column halves of a step are double-buffered
+// in registers: the reads of one half are issued before the MFMAs of the other, so LDS latency
+// hides under 16 MFMAs.  The DMA ring keeps RING stages occupied: right after the barrier that
+// ends the reads of stage kt, stage kt + RING is issued into its slot.  When the hidden size
+// spans at least RING stages, the stages issued in the last iterations of a tile are the first
+// stages of the workgroup's next tile (the ring slot of a stage is its index in the workgroup's
+// whole sequence modulo RING), so the next tile's operands arrive while this tile finishes and
+// runs its epilogue.
+template <int BM, int RING, bool kTop2>
+__global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
-    int vocab, int n_vtiles, int n_rtiles, int n_bands, Partial* __restrict__ part,
+    int vocab, int n_vtiles, int n_rtiles, Partial* __restrict__ part,
     float* __restrict__ part2) {
-  constexpr int BM = kTileBM, BN = 256, BK = kTileBK;
+  constexpr int BN = kTileBN, BK = kTileBK;
   constexpr int WM = 2, WN = 2, kWaves = WM * WN;
   constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
   constexpr int TM = kWaveM / 32, TN = kWaveN / 32;
@@ -496,50 +511,71 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
   constexpr int kStageBytes = (BM + BN) * kRowB;  // 32 KB
   constexpr int kInst = (BM + BN) / 16;           // 1 KB wave instructions per stage
   constexpr int kInstPerWave = kInst / kWaves;    // 8
+  constexpr int kRedBytes = WM * BN * (sizeof(Partial) + 4);
   static_assert(RING >= 2 && RING <= 4, "ring of 2 to 4 stages");
+  static_assert(kInst % kWaves == 0, "stage loads split evenly over the waves");
+  static_assert(RING * kStageBytes + kRedBytes <= 160 * 1024, "ring and reduction fit in LDS");
   static_assert((RING - 1) * kInstPerWave < 64, "vmcnt range");
-  __shared__ __attribute__((aligned(16))) uint8_t smem[RING * kStageBytes];
-  static_assert(WM * BN * sizeof(Partial) <= RING * kStageBytes, "reduction fits in the ring");
+  __shared__ __attribute__((aligned(16))) uint8_t smem[RING * kStageBytes + kRedBytes];
 
-  const int id = blockIdx.x;
-  const int xcd = id % kXcds, k = id / kXcds;
-  const int per_band = kBand * n_rtiles;
-  const int band = xcd + kXcds * (k / per_band);
-  if (band >= n_bands) return;
-  const int tt = k % per_band;
-  const int nv = min(kBand, n_vtiles - band * kBand);
-  if (tt >= nv * n_rtiles) return;
-  const int vt = band * kBand + tt % nv;
-  const int rt = tt / nv;
-  const int v0 = vt * BM, r0 = rt * BN;
+  // this workgroup's tiles: s0, s0 + step, ... below s_end
+  const int n_tiles = n_vtiles * n_rtiles;
+  const int g = blockIdx.x, groups = gridDim.x;
+  int s0 = g, step = groups, s_end = n_tiles;
+  if (groups == kTileGroups) {
+    const int x = g % kXcds;
+    s_end = static_cast<int>(static_cast<long long>(n_tiles) * (x + 1) / kXcds);
+    s0 = static_cast<int>(static_cast<long long>(n_tiles) * x / kXcds) + g / kXcds;
+    step = kTileGroups / kXcds;
+  }
+  if (s0 >= s_end) return;  // whole workgroup
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
   const int half = lane >> 5, l32 = lane & 31;
+  const int nk = hidden / BK;    // >= 2 (hidden is a multiple of 64)
+  const bool chain = nk >= RING;  // the tail of a tile issues the next tile's first stages
 
   // Load instruction i of this wave covers tile rows 16 q .. 16 q + 15, q = wave * 8 + i (rows
-  // below BM are W, the rest h); lane L fetches row 16 q + L / 4, global chunk
-  // (L % 4) ^ swizzle(row) into LDS slot L % 4 of the row.  Rows past the end are clamped.
-  const uint16_t* src[kInstPerWave];
+  // below BM are W, the rest h, so a wave loads from one operand only); lane L fetches row
+  // 16 q + L / 4, global chunk (L % 4) ^ swizzle(row) into LDS slot L % 4 of the row.  Rows past
+  // the end are clamped.  The loads are buffer loads into LDS: a resource per tile (its first
+  // row of the operand) in scalar registers, a byte offset per load instruction in a vector
+  // register, and the stage's column offset as the scalar offset.  (Global loads into LDS would
+  // count on the LDS-read counter as well, and the compiler then waits for every outstanding
+  // fragment read before each use of one.)
+  static_assert((BM / 16) % kInstPerWave == 0, "a wave loads from one operand");
+  const bool w_wave = __builtin_amdgcn_readfirstlane(wave) * kInstPerWave * 16 < BM;
+  struct Src {
+    __amdgpu_buffer_rsrc_t rs;
+    uint32_t off[kInstPerWave];
+  };
+  auto set_src = [&](Src& d, int vt_, int rt_) {
+    const uint16_t* base =
+        w_wave ? w + static_cast<size_t>(vt_) * BM * hidden : h + static_cast<size_t>(rt_) * BN * hidden;
+    const int last = w_wave ? vocab - 1 - vt_ * BM : n_rows - 1 - rt_ * BN;  // >= 0
+    d.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, 0x7fffffff,
+                                             kBufferWord3);
 #pragma unroll
-  for (int i = 0; i < kInstPerWave; ++i) {
-    const int q = wave * kInstPerWave + i;
-    const int row = 16 * q + (lane >> 2);
-    const int chunk = (lane & 3) ^ ((row >> 2) & 3);
-    src[i] = row < BM
-                 ? w + static_cast<size_t>(min(v0 + row, vocab - 1)) * hidden + chunk * 8
-                 : h + static_cast<size_t>(min(r0 + row - BM, n_rows - 1)) * hidden + chunk * 8;
-  }
-  // Stage `stage` of the k loop into ring slot `slot`.
-  auto issue = [&](int stage, int slot) {
+    for (int i = 0; i < kInstPerWave; ++i) {
+      const int q = wave * kInstPerWave + i;
+      const int row = 16 * q + (lane >> 2);
+      const int chunk = (lane & 3) ^ ((row >> 2) & 3);
+      const int r = min(w_wave ? row : row - BM, last);
+      d.off[i] = static_cast<uint32_t>(r * hidden * 2 + chunk * 16);
+    }
+  };
+  // Stage `stage` of the tile described by d, into ring slot `slot`.
+  auto issue = [&](const Src& d, int stage, int slot) {
     uint8_t* base = smem + slot * kStageBytes;
 #pragma unroll
     for (int i = 0; i < kInstPerWave; ++i)
-      load_to_lds(src[i] + stage * BK, base + (wave * kInstPerWave + i) * 1024);
+      buffer_load_to_lds(d.rs, base + (wave * kInstPerWave + i) * 1024, d.off[i], stage * BK * 2);
   };
-  // Fragments of half s (k columns 16 s .. 16 s + 15 of the stage, chunk 2 half + s per lane).
-  auto read = [&](int kt, int s, bf16x8 (&a)[TM], bf16x8 (&b)[TN]) {
-    const uint8_t* st = smem + (kt % RING) * kStageBytes;
+  // Fragments of half s (k columns 16 s .. 16 s + 15 of the stage in ring slot `slot`, chunk
+  // 2 half + s per lane).
+  auto read = [&](int slot, int s, bf16x8 (&a)[TM], bf16x8 (&b)[TN]) {
+    const uint8_t* st = smem + slot * kStageBytes;
     const int c = 2 * half + s;
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
@@ -554,109 +590,162 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile4_kernel(
   };
 
   f32x16 acc[TM][TN];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < TN; ++b) acc[a][b] = f32x16{};
   auto mma = [&](const bf16x8 (&a)[TM], const bf16x8 (&b)[TN]) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32(a[tm], b[tn], acc[tm][tn]);
   };
-  // Every iteration issues exactly one stage (past the end: the last stage again, into the slot
-  // just freed, never read), so the number of younger stages in flight at each barrier is
-  // always RING - 2 and every wait is the same; straight-line code lets the fragment reads of
-  // one half stay in flight under the MFMAs of the other.
-  const int nk = hidden / BK;  // >= 1
-#pragma unroll
-  for (int j = 0; j < RING; ++j) issue(min(j, nk - 1), j);
-  wait_vm_lds_and_barrier<(RING - 1) * kInstPerWave>();
-  bf16x8 xa[TM], xb[TN], ya[TM], yb[TN];
-  read(0, 0, xa, xb);
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    read(kt, 1, ya, yb);
-    mma(xa, xb);
-    // one fragment read after each of the first 8 MFMAs
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm_lds_and_barrier<(RING - 2) * kInstPerWave>();  // stage kt + 1 has landed
-    issue(min(kt + RING, nk - 1), kt % RING);               // slot of stage kt, fully read
-    read(kt + 1, 0, xa, xb);
-    mma(ya, yb);
-    // one DMA load after each of the first 8 MFMAs, one fragment read after each of the rest
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  read(nk - 1, 1, ya, yb);
-  mma(xa, xb);
-  mma(ya, yb);
-  wait_vm_lds_and_barrier<0>();  // no DMA in flight; every wave is done reading the ring
-
-  Partial* red = reinterpret_cast<Partial*>(smem);  // [WM][BN]
+  Partial* red = reinterpret_cast<Partial*>(smem + RING * kStageBytes);  // [WM][BN]
   float* red2 = reinterpret_cast<float*>(red + WM * BN);
-  static_assert(WM * BN * (sizeof(Partial) + 4) <= sizeof(smem), "reduction fits in LDS");
-  const bool full = v0 + BM <= vocab;
-  const int vbase = v0 + wm * kWaveM + 4 * half;
+
+  int s = s0, vt, rt;
+  band_tile(s, n_vtiles, n_rtiles, vt, rt);
+  Src src, nsrc;
+  set_src(src, vt, rt);
+  int slot0 = 0;  // ring slot of the current tile's stage 0
 #pragma unroll
-  for (int tn = 0; tn < TN; ++tn) {
-    float m2 = kNegBig;
-    Partial p = column_partial<TM, TN, kTop2>(acc, tn, vbase, vocab, full, &m2);
-    if (kTop2) m2 = top2_shfl_merge(p.m, m2, 32);
-    p = partial_xor_merge(p, 32, lane);
-    if (lane < 32) {
-      red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
-      if (kTop2) red2[wm * BN + wn * kWaveN + tn * 32 + l32] = m2;
+  for (int j = 0; j < RING; ++j) issue(src, min(j, nk - 1), j);
+  constexpr int kReads = TM + TN, kMfmas = TM * TN;
+  static_assert(kInstPerWave + kReads <= kMfmas, "loads and reads interleave with the MFMAs");
+  for (;;) {
+    const int ns = s + step;
+    const bool next = ns < s_end;
+    int nvt = 0, nrt = 0;
+    if (next) {
+      band_tile(ns, n_vtiles, n_rtiles, nvt, nrt);
+      set_src(nsrc, nvt, nrt);
     }
-  }
-  __syncthreads();
-  for (int c = tid; c < BN; c += kWaves * 64) {
-    Partial p = red[c];
-    float m2 = kTop2 ? red2[c] : kNegBig;
+    const bool pre = next && chain;
+    auto slot = [&](int kt) { return (slot0 + kt) % RING; };
+
 #pragma unroll
-    for (int q = 1; q < WM; ++q) {
-      const Partial o = red[q * BN + c];
-      if (kTop2) m2 = top2_merge(p.m, m2, o.m, red2[q * BN + c]);
-      p = partial_merge(p, o);
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b) acc[a][b] = f32x16{};
+    // Every iteration issues exactly one stage (this tile's stage kt + RING, else the next
+    // tile's, else this tile's last stage again into the slot just freed, never read), so the
+    // number of younger stages in flight at each barrier is always RING - 2 and every wait is
+    // the same; straight-line code lets the fragment reads of one half stay in flight under the
+    // MFMAs of the other.
+    wait_vm_lds_and_barrier<(RING - 1) * kInstPerWave>();  // stage 0 has landed
+    bf16x8 xa[TM], xb[TN], ya[TM], yb[TN];
+    read(slot(0), 0, xa, xb);
+    // Step kt: half 1 of stage kt, the barrier, then stage `stage` of the tile at p into the
+    // slot of stage kt + RING (the slot stage kt just freed) and half 2 of stage kt.
+    auto body = [&](int kt, const Src& p, int stage) {
+      read(slot(kt), 1, ya, yb);
+      mma(xa, xb);
+      // one fragment read after each of the first kReads MFMAs
+#pragma unroll
+      for (int i = 0; i < kReads; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfmas - kReads, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vm_lds_and_barrier<(RING - 2) * kInstPerWave>();  // stage kt + 1 has landed
+      issue(p, stage, slot(kt + RING));
+      read(slot(kt + 1), 0, xa, xb);
+      mma(ya, yb);
+      // one DMA load after each of the first kInstPerWave MFMAs, one fragment read after each
+      // of the next kReads
+#pragma unroll
+      for (int i = 0; i < kInstPerWave; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < kReads; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      if constexpr (kMfmas > kInstPerWave + kReads)
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmas - kInstPerWave - kReads, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    // Every step issues exactly one stage: this tile's stage kt + RING while there is one,
+    // then the next tile's first stages (or, without a next tile or with fewer than RING
+    // stages per tile, this tile's last stage again into the slot just freed, never read).  So
+    // the number of younger stages in flight at each barrier is always RING - 2 and every wait
+    // is the same; straight-line steps let the fragment reads of one half stay in flight under
+    // the MFMAs of the other.
+    int kt = 0;
+    for (; kt + RING < nk; ++kt) body(kt, src, kt + RING);
+    const Src& tsrc = pre ? nsrc : src;
+    for (; kt + 1 < nk; ++kt) body(kt, tsrc, pre ? kt + RING - nk : nk - 1);
+    read(slot(nk - 1), 1, ya, yb);
+    mma(xa, xb);
+    mma(ya, yb);
+    if (pre) {
+      // every wave is done reading the ring; the next tile's stage RING - 1 goes into the slot
+      // of this tile's last stage (its stages 0 .. RING - 2 are in flight already)
+      wait_vm_lds_and_barrier<63>();
+      issue(nsrc, RING - 1, slot(nk + RING - 1));
+    } else {
+      wait_vm_lds_and_barrier<0>();  // no DMA in flight; every wave is done reading the ring
     }
-    const int row = r0 + c;
-    if (row < n_rows) {
-      part[static_cast<size_t>(row) * n_vtiles + vt] = p;
-      if (kTop2) part2[static_cast<size_t>(row) * n_vtiles + vt] = m2;
+
+    const bool full = vt * BM + BM <= vocab;
+    const int vbase = vt * BM + wm * kWaveM + 4 * half;
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      float m2 = kNegBig;
+      Partial p = column_partial<TM, TN, kTop2>(acc, tn, vbase, vocab, full, &m2);
+      if (kTop2) m2 = top2_shfl_merge(p.m, m2, 32);
+      p = partial_xor_merge(p, 32, lane);
+      if (lane < 32) {
+        red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
+        if (kTop2) red2[wm * BN + wn * kWaveN + tn * 32 + l32] = m2;
+      }
+    }
+    __syncthreads();
+    for (int c = tid; c < BN; c += kWaves * 64) {
+      Partial p = red[c];
+      float m2 = kTop2 ? red2[c] : kNegBig;
+#pragma unroll
+      for (int q = 1; q < WM; ++q) {
+        const Partial o = red[q * BN + c];
+        if (kTop2) m2 = top2_merge(p.m, m2, o.m, red2[q * BN + c]);
+        p = partial_merge(p, o);
+      }
+      const int row = rt * BN + c;
+      if (row < n_rows) {
+        part[static_cast<size_t>(row) * n_vtiles + vt] = p;
+        if (kTop2) part2[static_cast<size_t>(row) * n_vtiles + vt] = m2;
+      }
+    }
+    if (!next) break;
+    s = ns;
+    vt = nvt;
+    rt = nrt;
+    src = nsrc;
+    if (pre) {
+      slot0 = (slot0 + nk) % RING;
+    } else {
+      slot0 = 0;
+#pragma unroll
+      for (int j = 0; j < RING; ++j) issue(src, min(j, nk - 1), j);
     }
   }
 }
 
-// Tile kernel of the large-batch path: lmhead_tile4_kernel, 256 x 256 tiles, 4 waves of
-// 128 x 128, ring of 4 (128 KB LDS, one workgroup per compute unit); batch 64: 9.6 ms.
+// Tile kernel of the large-batch path: 256 x 256 tiles, 4 waves of 128 x 128, ring of 4
+// (128 KB LDS, one workgroup per compute unit).
 // Measured and dropped: 8 waves of 128 x 64 (10.55 ms), 256 x 128 tiles with a ring of 3 at two
 // workgroups per compute unit (11.8 ms), stages reaching LDS through registers (9.65 ms),
 // 64-column stages with one barrier per 64 MFMAs (10.1 ms), DMA loads spread over both halves of
-// a step (no change); with every operand L2-resident the kernel runs at the same speed, so it is
-// bound by the issue/LDS schedule of one wave per SIMD, not by memory.
-constexpr int kTileBN = 256;
-
+// a step (no change), 384 x 256 tiles (384 accumulators per lane: the compiler spills).
 template <bool kTop2>
 hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const void* w,
                        Partial* part, float* part2, hipStream_t s) {
-  const TileMap m = tile_map(n_rows, vocab, kTileBN);
-  hipLaunchKernelGGL((lmhead_tile4_kernel<4, kTop2>), dim3(m.grid), dim3(256), 0, s,
-                     static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w), n_rows,
-                     hidden, vocab, m.n_vtiles, m.n_rtiles, m.n_bands, part, part2);
+  const int n_vtiles = tile_vtiles(vocab);
+  const int n_rtiles = (n_rows + kTileBN - 1) / kTileBN;
+  const int n_tiles = n_vtiles * n_rtiles;
+  const int groups = n_tiles >= kTileGroups ? kTileGroups : n_tiles;
+  hipLaunchKernelGGL((lmhead_tile_kernel<kTileBM, kTileRing, kTop2>), dim3(groups), dim3(256), 0,
+                     s, static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w), n_rows,
+                     hidden, vocab, n_vtiles, n_rtiles, part, part2);
   return hipGetLastError();
 }
 
@@ -752,7 +841,7 @@ __global__ __launch_bounds__(256) void lmhead_combine_kernel(const Partial* __re
 
 int lmhead_num_slices(bool bf16, int n_rows, int vocab) {
   if (bf16 && use_stream(n_rows, vocab)) return stream_plan(vocab).groups;
-  if (bf16) return tile_map(n_rows, vocab, kTileBN).n_vtiles;
+  if (bf16) return tile_vtiles(vocab);
   return (vocab + kF32SliceRows - 1) / kF32SliceRows;
 }
 

@@ -63,6 +63,12 @@ LM_CASES = [
     # large-batch kernel: several row tiles, vocabulary bands with a partial last band
     (600, 192, 9000, "bf16"),
     (300, 128, 1100, "bf16"),
+    # more tiles than persistent workgroups: several tiles per workgroup, the next tile's first
+    # stages issued in the previous tile's tail (hidden of exactly 4 stages; 6 stages, so the
+    # ring position of a tile's first stage moves), or not (hidden of 2 stages)
+    (300, 128, 70000, "bf16"),
+    (1100, 192, 100000, "bf16"),
+    (700, 64, 40000, "bf16"),
     # streaming kernel: 16 waves with 1..3 row tiles each, 8 waves with 7 or 8, partial h chunks
     (32, 256, 126464, "bf16"),
     (17, 128, 152064, "bf16"),
