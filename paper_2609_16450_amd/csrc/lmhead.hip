@@ -422,20 +422,24 @@ __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], i
   if (kTop2)
     *m2 = top2_merge(fmaxf(mc[0], mc[1]), top2_merge(mc[0], mc2[0], mc[1], mc2[1]),
                      fmaxf(mc[2], mc[3]), top2_merge(mc[2], mc2[2], mc[3], mc2[3]));
+  // The argmax of chain c is tracked as k = 4 tm + r / 4 (o = 8 k + c), a small constant that
+  // the select instruction takes inline; kNoK marks "not seen".
+  constexpr int kNoK = 4 * TM;
   float sc[4] = {0.f, 0.f, 0.f, 0.f}, tc[4] = {0.f, 0.f, 0.f, 0.f};
-  int32_t oc[4] = {kNoIndex, kNoIndex, kNoIndex, kNoIndex};
+  int32_t kc[4] = {kNoK, kNoK, kNoK, kNoK};
 #pragma unroll
   for (int tm = TM - 1; tm >= 0; --tm)
 #pragma unroll
     for (int r = 15; r >= 0; --r) {
       const int o = tm * 32 + 8 * (r >> 2) + (r & 3);
+      const int k = 4 * tm + (r >> 2);
       const float z = acc[tm][tn][r];
       if (kFull) {
         const float y = (z - m) * kLog2e;
         const float e = fast_exp2(y);
         sc[r & 3] += e;
         tc[r & 3] = fmaf(e, y, tc[r & 3]);
-        oc[r & 3] = z == m ? o : oc[r & 3];
+        kc[r & 3] = z == m ? k : kc[r & 3];
       } else {
         const bool ok = vbase + o < vocab;
         // rows past the vocabulary contribute e = 0 and y = 0 (a lane with no valid row keeps
@@ -444,10 +448,12 @@ __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], i
         const float e = ok ? fast_exp2(y) : 0.f;
         sc[r & 3] += e;
         tc[r & 3] = fmaf(e, y, tc[r & 3]);
-        oc[r & 3] = (ok && z == m) ? o : oc[r & 3];
+        kc[r & 3] = (ok && z == m) ? k : kc[r & 3];
       }
     }
-  const int32_t ob = min(min(oc[0], oc[1]), min(oc[2], oc[3]));
+  int32_t ob = kNoIndex;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) ob = min(ob, kc[c] == kNoK ? kNoIndex : 8 * kc[c] + c);
   return Partial{m, (sc[0] + sc[1]) + (sc[2] + sc[3]), (tc[0] + tc[1]) + (tc[2] + tc[3]),
                  ob == kNoIndex ? kNoIndex : vbase + ob};
 }
