@@ -43,6 +43,41 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
+// acc + lo + hi of the two bf16 values packed in w (one dot instruction against (1, 1)).  Takes
+// the word as a scalar: the front end lowers a bit cast of a vector-element expression
+// (__builtin_bit_cast(T, v[i])) to element 0 whatever i is.
+__device__ __forceinline__ float sum2_bf16(uint32_t w, float acc) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w),
+                                         __builtin_bit_cast(bf16x2, 0x3f803f80u), acc, false);
+}
+
+// Buffer loads straight into LDS.  A raw buffer resource over memory starting at `base` (2 GiB
+// range, word 3 as gfx9 raw dword loads need); 16 bytes per lane from byte offset voff + soff
+// into LDS at l + 16 * lane (the LDS address is wave-uniform).  The builtins sit in device
+// functions of their own: inside a kernel body the host compilation would drop the kernel.
+// (Loads into LDS issued as global loads count on the LDS-read counter as well, and the
+// compiler then waits for every outstanding LDS read before each use of one; buffer loads do
+// not.)
+typedef __attribute__((address_space(3))) void lds_void_t;
+constexpr int kBufferWord3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7fffffff, kBufferWord3);
+}
+__device__ __forceinline__ void buffer_load_to_lds(__amdgpu_buffer_rsrc_t rs, void* l,
+                                                   uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(l), 16, voff, soff, 0, 0);
+}
+
+// Wait until at most N vector-memory instructions of this wave are outstanding and all of its
+// LDS reads have returned, then barrier.
+template <int N>
+__device__ __forceinline__ void wait_vm_lds_and_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0x0 << 8));
+  asm volatile("s_barrier" ::: "memory");
+}
+
 // bf16 <-> f32
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t u) {
   return __uint_as_float(static_cast<uint32_t>(u) << 16);

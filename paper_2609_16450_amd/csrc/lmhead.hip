@@ -378,19 +378,10 @@ constexpr int kTileBN = 256;     // block positions per tile
 constexpr int kTileBK = 32;      // hidden columns per ring stage
 constexpr int kTileRing = 4;     // ring stages
 constexpr int kTileGroups = 256; // persistent workgroups (one per compute unit)
-constexpr int kBufferWord3 = 0x00020000;  // buffer resource word 3 for raw dword loads on gfx9
 
 int tile_vtiles(int vocab) { return (vocab + kTileBM - 1) / kTileBM; }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
 
-// 16 bytes per lane from buffer rs at byte offset voff + soff into LDS at l + 16 * lane (a
-// buffer load straight into LDS; the LDS address is wave-uniform).  The builtin sits in a
-// device function of its own: inside a kernel body the host compilation would drop the kernel.
-__device__ __forceinline__ void buffer_load_to_lds(__amdgpu_buffer_rsrc_t rs, void* l,
-                                                   uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(l), 16, voff, soff, 0, 0);
-}
 
 // Partial statistics of one lane's column over TM 32-row MFMA blocks.  Element (tm, r) of the
 // lane is vocabulary row vbase + o with o = 32 tm + 8 (r / 4) + (r % 4).  Four independent chains
@@ -464,15 +455,6 @@ __device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], i
                                                   int vocab, bool full, float* m2) {
   return full ? column_partial<TM, TN, kTop2, true>(acc, tn, vbase, vocab, m2)
               : column_partial<TM, TN, kTop2, false>(acc, tn, vbase, vocab, m2);
-}
-
-// Wait until at most N vector-memory instructions of this wave are outstanding and all of its
-// LDS reads have returned, then barrier.
-template <int N>
-__device__ __forceinline__ void wait_vm_lds_and_barrier() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0x0 << 8));
-  asm volatile("s_barrier" ::: "memory");
 }
 
 // Tile (vt, rt) of position s of the launch sequence: bands of kBand vocabulary tiles (the last
@@ -560,8 +542,7 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
     const uint16_t* base =
         w_wave ? w + static_cast<size_t>(vt_) * BM * hidden : h + static_cast<size_t>(rt_) * BN * hidden;
     const int last = w_wave ? vocab - 1 - vt_ * BM : n_rows - 1 - rt_ * BN;  // >= 0
-    d.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, 0x7fffffff,
-                                             kBufferWord3);
+    d.rs = make_rsrc(base);
 #pragma unroll
     for (int i = 0; i < kInstPerWave; ++i) {
       const int q = wave * kInstPerWave + i;
