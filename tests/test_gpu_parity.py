@@ -21,7 +21,7 @@ from paper_2609_16450_amd import (EB_BF16, Ragged, eb_block_attn, eb_decode_step
                                   eb_lmhead_confidence, eb_unmask_select)
 from paper_2609_16450_amd.device_case import DeviceStep
 from tests._cases import as_f32, enforce_margins
-from workloads import CONFIGS, custom_config, make_step
+from workloads import CONFIGS, custom_config, make_step, f32_to_bf16_bits, bf16_bits_to_f32
 
 pytestmark = pytest.mark.gpu
 
@@ -166,6 +166,35 @@ def test_block_attn_small(batch, hq, hkv, D, bl, pl, dt):
     torch.cuda.synchronize()
     tol = ATTN_TOL_BF16 if dt == "bf16" else ATTN_TOL_F32
     np.testing.assert_allclose(attn_out_f32(ds.attn_out), ref, **tol)
+
+
+@pytest.mark.parametrize("split", [False, True])
+def test_block_attn_scores_growing_along_the_keys(split):
+    # Keys scaled up along each sequence, so the running maximum of a row keeps moving by more
+    # than the kernel's rescale slack (2^8) from tile to tile; with split the key ranges are
+    # merged from partials (batch 1: the split plan cuts the keys to fill the chip).
+    # batch 16 x 4 K/V heads x 7 row tiles: two key ranges of ~8 tiles per workgroup;
+    # batch 2: one or two tiles per range
+    batch, hq, hkv = (2, 8, 2) if split else (16, 28, 4)
+    say(f"attn growing scores split={split}")
+    cfg = custom_config(seed=4242 + batch, batch=batch, hq=hq, hkv=hkv, head_dim=128,
+                        block_len=("fixed", 128), prefix_len=("uniform", 500, 900),
+                        hidden=64, vocab=64, dtype="bf16")
+    case = make_step(cfg)
+    for b in range(case.batch):
+        p0, p1 = case.cu_prefix[b], case.cu_prefix[b + 1]
+        ramp = (1.0 + 9.0 * np.arange(p1 - p0) / max(1, p1 - p0)).astype(np.float32)
+        k = bf16_bits_to_f32(case.k_pre[p0:p1]) * ramp[:, None, None]
+        case.k_pre[p0:p1] = f32_to_bf16_bits(k)
+        b0, b1 = case.cu_block[b], case.cu_block[b + 1]
+        case.k_blk[b0:b1] = f32_to_bf16_bits(bf16_bits_to_f32(case.k_blk[b0:b1]) * 10.0)
+    f = {k: as_f32(getattr(case, k), "bf16") for k in ("q", "k_blk", "v_blk", "k_pre", "v_pre")}
+    ref = oracle.block_attention(**f, cu_block=case.cu_block, cu_prefix=case.cu_prefix,
+                                 hq=hq, hkv=hkv)
+    ds = DeviceStep(case)
+    eb_block_attn(ds.ragged, ds.q, ds.k_blk, ds.v_blk, ds.k_pre, ds.v_pre, ds.attn_out)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(attn_out_f32(ds.attn_out), ref, **ATTN_TOL_BF16)
 
 
 # ----------------------------------------------------------------------------------------
