@@ -77,7 +77,7 @@ def lmhead_kernel_name(dtype: str, T: int) -> str:
     bf16 rows, the tile kernel above)."""
     if dtype == "f32":
         return "lmhead_f32_kernel"
-    return "lmhead_stream16_kernel" if T <= 64 else "lmhead_tile4_kernel"
+    return "lmhead_stream16_kernel" if T <= 64 else "lmhead_tile_kernel"
 
 
 def measured_traffic(workload: str):
