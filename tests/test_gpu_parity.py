@@ -287,8 +287,19 @@ def _sample_blocks(case, k=3):
 
 @pytest.mark.parametrize("name", list(CONFIGS))
 def test_decode_step_workload(name):
-    say(f"decode_step workload={name}")
-    case = make_step(name)
+    _check_workload(name, None)
+
+
+# the two small workloads also on further seeds (other block contents, masks and runs)
+@pytest.mark.parametrize("name,seed", [(n, s) for n in ("tiny_f32_b1", "llada8b_b1")
+                                       for s in (1, 2, 3)])
+def test_decode_step_workload_other_seeds(name, seed):
+    _check_workload(name, seed)
+
+
+def _check_workload(name, seed):
+    say(f"decode_step workload={name} seed={seed}")
+    case = make_step(name, seed)
     full = case.T <= 64
     blocks = list(range(case.batch)) if full else _sample_blocks(case)
     enforce_margins(case, blocks)
