@@ -359,17 +359,17 @@ hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, 
 // ---------------------------------------------------------------------------------------
 // Large-batch kernel: 256 (vocabulary) x 256 (positions) tiles.
 //
-// Both operands are streamed HBM -> LDS by direct loads (global_load_lds_dwordx4: lane l of a
-// wave writes its 16 bytes to LDS base + 16 l) into a ring of RING stages of BK = 32 hidden
-// columns, RING - 1 stages in flight; no staging registers and no LDS store instructions.  LDS
-// rows are 64 bytes without padding; the 16-byte chunk c of row r is kept in slot
-// c ^ ((r / 4) % 4), which makes the 32-row MFMA operand reads free of bank conflicts.
-// Four waves form a 2 x 2 grid of 128 x 128 sub-tiles of 32x32x16 MFMA blocks.
+// Both operands go HBM/L2 -> LDS by buffer loads straight into LDS (lane l of a wave writes its
+// 16 bytes to LDS base + 16 l) into a ring of RING stages of BK = 32 hidden columns, RING - 1
+// stages in flight; no staging registers and no LDS store instructions.  LDS rows are 64 bytes
+// without padding; the 16-byte chunk c of row r is kept in slot c ^ ((r / 4) % 4), which makes
+// the 32-row MFMA operand reads free of bank conflicts.  Four waves form a 2 x 2 grid of
+// 128 x 128 sub-tiles of 32x32x16 MFMA blocks.
 //
-// Launch order is XCD-aware: vocabulary tiles are grouped in bands of kBand, band b goes to XCD
-// b % 8 (workgroups are dealt to the 8 XCDs round-robin by id), and each XCD sweeps its band row
-// tile by row tile, so the workgroups an XCD runs at once share a few W and h tiles in its L2
-// and each W tile is fetched from HBM about once.
+// Tile order is XCD-aware: the launch sequence takes vocabulary tiles in bands of kBand, each
+// band swept position tile by position tile, and is cut into one contiguous segment per XCD
+// (lmhead_tile_kernel), so the workgroups an XCD runs at once work on neighbouring tiles that
+// share a few W and h tiles in its L2.
 // ---------------------------------------------------------------------------------------
 constexpr int kXcds = 8;
 constexpr int kBand = 4;
