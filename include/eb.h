@@ -30,7 +30,10 @@
  *     variable EB_DEBUG_CHECKS (any value but "0") makes every entry point that takes cu
  *     arrays or tau copy them to the host after the work already on its stream (which
  *     synchronises that stream) and return EB_ERR_INVALID, launching nothing, when they break
- *     this contract.  Such calls cannot be captured in a graph.
+ *     this contract.  Such calls cannot be captured in a graph.  For testing, the environment
+ *     variable EB_ATTN_STAGED (any value but "0") makes the bf16 attention at head dimension
+ *     128 use the kernel it otherwise keeps for K/V segments too long for 32-bit offsets;
+ *     results agree with the default kernel to the attention tolerance, not bit for bit.
  *   - Rows are packed: the block rows of sequence b are rows cu_block[b] .. cu_block[b+1]-1,
  *     in ascending sequence position (a non-contiguous block is gathered in order), its
  *     cached prefix rows are cu_prefix[b] .. cu_prefix[b+1]-1.  Empty blocks are legal.

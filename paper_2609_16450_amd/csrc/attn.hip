@@ -13,6 +13,9 @@
 // registers, V stored transposed in LDS).
 // Small steps (attn_small_ok) take the 16-row role of attn_small.hpp instead, here as a kernel
 // of its own; the decode step runs the same role inside the LM-head launch.
+#include <cstdlib>
+#include <cstring>
+
 #include "attn_common.hpp"
 #include "attn_small.hpp"
 #include "eb_common.hpp"
@@ -698,6 +701,14 @@ inline bool attn_dma_offsets_fit(const AttnArgs& a) {
   return longest * key_bytes < (1L << 31);
 }
 
+// EB_ATTN_STAGED (any value but "0") sends head dimension 128 to attn_bf16_kernel<128>, the
+// form the library otherwise keeps for segments too long for 32-bit buffer offsets, so that
+// it can be tested at ordinary sizes.
+inline bool attn_force_staged() {
+  const char* v = getenv("EB_ATTN_STAGED");
+  return v && *v && strcmp(v, "0") != 0;
+}
+
 }  // namespace
 
 size_t block_attn_ws_bytes(bool bf16, bool allow_split, int batch, int total_block, int max_block,
@@ -740,7 +751,7 @@ hipError_t block_attn(bool bf16, bool allow_split, const AttnArgs& a, void* ws, 
     const int units = a.batch * sp.nsplit * a.hkv;
     const dim3 grid(static_cast<unsigned>(kXcdCount * ((units + kXcdCount - 1) / kXcdCount) *
                                           row_tiles));
-    if (a.head_dim == 128 && attn_dma_offsets_fit(a))
+    if (a.head_dim == 128 && attn_dma_offsets_fit(a) && !attn_force_staged())
       hipLaunchKernelGGL(attn_bf16_d128_kernel, grid, dim3(kThreads), 0, s, p, row_tiles, units);
     else if (a.head_dim == 128)
       hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kThreads), 0, s, p, row_tiles, units);

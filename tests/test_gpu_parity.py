@@ -168,8 +168,22 @@ def test_block_attn_small(batch, hq, hkv, D, bl, pl, dt):
     np.testing.assert_allclose(attn_out_f32(ds.attn_out), ref, **tol)
 
 
+# head dimension 128, not small: the register-staged kernel the library keeps for K/V segments
+# too long for 32-bit buffer offsets, selected here by EB_ATTN_STAGED
+STAGED_CASES = [c for c in ATTN_CASES if c[3] == 128 and c[6] == "bf16"]
+
+
+@pytest.mark.parametrize("batch,hq,hkv,D,bl,pl,dt", STAGED_CASES)
+def test_block_attn_register_staged_form(batch, hq, hkv, D, bl, pl, dt, monkeypatch):
+    monkeypatch.setenv("EB_ATTN_STAGED", "1")
+    test_block_attn_small(batch, hq, hkv, D, bl, pl, dt)
+
+
+@pytest.mark.parametrize("staged", [False, True])
 @pytest.mark.parametrize("split", [False, True])
-def test_block_attn_scores_growing_along_the_keys(split):
+def test_block_attn_scores_growing_along_the_keys(split, staged, monkeypatch):
+    if staged:
+        monkeypatch.setenv("EB_ATTN_STAGED", "1")
     # Keys scaled up along each sequence, so the running maximum of a row keeps moving by more
     # than the kernel's rescale slack (2^8) from tile to tile; with split the key ranges are
     # merged from partials (batch 1: the split plan cuts the keys to fill the chip).
