@@ -92,8 +92,9 @@ typedef struct {
  *
  * Requires hq % hkv == 0, head_dim in {64, 128}, scale > 0 and finite; scale = 0 selects
  * 1/sqrt(head_dim) (rounded to fp32, the same bits eb_decode_step uses for attn_scale <= 0).
- * Arithmetic: bf16 inputs, fp32 scores / softmax / accumulation, output rounded to bf16
- * (round to nearest even); EB_F32 computes in fp32 throughout.
+ * Arithmetic: bf16 inputs, fp32 scores / softmax / accumulation, the probabilities rounded to
+ * bf16 for the product with V (at head_dim 128 the softmax denominator sums those same rounded
+ * values), output rounded to bf16 (round to nearest even); EB_F32 computes in fp32 throughout.
  * ------------------------------------------------------------------------------------- */
 size_t eb_block_attn_workspace(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim);
 eb_status eb_block_attn(eb_dtype dt, const eb_ragged* r, int hq, int hkv, int head_dim,
