@@ -373,9 +373,10 @@ def _check_workload(name, seed):
         assert (nc[b] >= 1) == m0[sl].any()
 
 
-def test_decode_step_is_deterministic():
-    say("determinism llada8b_b16")
-    case = make_step("llada8b_b16")
+@pytest.mark.parametrize("name", ["llada8b_b16", "dream7b_b64"])
+def test_decode_step_is_deterministic(name):
+    say(f"determinism {name}")
+    case = make_step(name)
     ds = DeviceStep(case)
     outs = []
     for _ in range(2):
