@@ -363,8 +363,8 @@ hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, 
 // 16 bytes to LDS base + 16 l) into a ring of RING stages of BK = 32 hidden columns, RING - 1
 // stages in flight; no staging registers and no LDS store instructions.  LDS rows are 64 bytes
 // without padding; the 16-byte chunk c of row r is kept in slot c ^ ((r / 4) % 4), which makes
-// the 32-row MFMA operand reads free of bank conflicts.  Four waves form a 2 x 2 grid of
-// 128 x 128 sub-tiles of 32x32x16 MFMA blocks.
+// the 16-row MFMA operand reads free of bank conflicts.  Four waves form a 2 x 2 grid of
+// 128 x 128 sub-tiles of 16x16x32 MFMA blocks.
 //
 // Tile order is XCD-aware: the launch sequence takes vocabulary tiles in bands of kBand, each
 // band swept position tile by position tile, and is cut into one contiguous segment per XCD
@@ -381,80 +381,115 @@ constexpr int kTileGroups = 256; // persistent workgroups (one per compute unit)
 
 int tile_vtiles(int vocab) { return (vocab + kTileBM - 1) / kTileBM; }
 
+// 16x16x32 MFMA with its accumulator tied to the same AGPRs as input and output.  Written as asm:
+// with the builtin, the compiler picks the untied form for this size and moves the accumulators
+// through other registers around every MFMA of a 64-accumulator loop (hundreds of copies per
+// step, seen in the ISA).
+__device__ __forceinline__ void mfma16_tied(f32x4& c, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
 
+// The compiler does not see that the asm above is an MFMA, so it inserts none of the wait states
+// between an MFMA and other instructions touching its accumulators.  Every accumulator passes
+// through an empty asm that "writes" it, which no access of it can cross, and s_nops supply the
+// wait states: acc_fence_in after the accumulators are written and before the first MFMA reads
+// them, acc_fence_out after the last MFMA and before anything reads its results.
+template <int TM, int TN>
+__device__ __forceinline__ void acc_fence_in(f32x4 (&acc)[TM][TN]) {
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b) asm volatile("" : "+a"(acc[a][b]));
+  asm volatile("s_nop 7");
+}
+template <int TM, int TN>
+__device__ __forceinline__ void acc_fence_out(f32x4 (&acc)[TM][TN]) {
+  asm volatile("s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7");
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b) asm volatile("" : "+a"(acc[a][b]));
+}
 
-// Partial statistics of one lane's column over TM 32-row MFMA blocks.  Element (tm, r) of the
-// lane is vocabulary row vbase + o with o = 32 tm + 8 (r / 4) + (r % 4).  Four independent chains
-// (by r % 4) carry the max, the sums and the first argmax, so the reduction is not bound by the
-// latency of one long dependency chain; each chain walks its rows in decreasing order, so its
-// last z == max hit is its lowest row, and the chains are combined at the end.  The argmax is
-// tracked as the offset o, a constant of the unrolled code, and kFull (every row inside the
-// vocabulary) drops the per-row bounds test: neither a row index nor a mask is then kept per
-// element.  With kTop2 the max pass also tracks each chain's second-largest logit; m2 returns
-// the lane's second-largest (kNegBig if none).
+// Statistics of one column of a wave's 16x16x32 accumulator tile: lane l holds, for column block
+// tn, vocabulary rows vbase + 16 tm + r (tm < TM, r < 4; vbase includes the lane's 4 (l / 16)) of
+// column l % 16, and the four lanes l % 16 + 16 q together hold the column's 16 TM rows.  A max
+// pass in four chains (by r), the column maximum M over the four lanes, one exponential pass
+// against M, then the four lanes' sums added by a butterfly (a + b on one lane, b + a on its
+// partner: identical bits on all four).  Each chain walks its rows in decreasing order, so its
+// last z == M is its lowest row; the argmax is kept as the block index tm, a constant of the
+// unrolled code.  kFull (every row inside the vocabulary) drops the per-row bounds test.  With
+// kTop2, m2 returns the column's second-largest logit (kNegBig if none).
 template <int TM, int TN, bool kTop2, bool kFull>
-__device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], int tn, int vbase,
+__device__ __forceinline__ Partial column_stats16(const f32x4 (&acc)[TM][TN], int tn, int vbase,
                                                   int vocab, float* m2) {
   float mc[4] = {kNegBig, kNegBig, kNegBig, kNegBig};
   float mc2[4] = {kNegBig, kNegBig, kNegBig, kNegBig};
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int o = tm * 32 + 8 * (r >> 2) + (r & 3);
-      if (kFull || vbase + o < vocab) {
+    for (int r = 0; r < 4; ++r) {
+      if (kFull || vbase + tm * 16 + r < vocab) {
         const float z = acc[tm][tn][r];
         // with mc >= mc2, the new second-largest is the median of (mc, mc2, z): one v_med3
-        if (kTop2) mc2[r & 3] = __builtin_amdgcn_fmed3f(mc[r & 3], mc2[r & 3], z);
-        mc[r & 3] = fmaxf(mc[r & 3], z);
+        if (kTop2) mc2[r] = __builtin_amdgcn_fmed3f(mc[r], mc2[r], z);
+        mc[r] = fmaxf(mc[r], z);
       }
     }
   const float m = fmaxf(fmaxf(mc[0], mc[1]), fmaxf(mc[2], mc[3]));
-  if (kTop2)
-    *m2 = top2_merge(fmaxf(mc[0], mc[1]), top2_merge(mc[0], mc2[0], mc[1], mc2[1]),
-                     fmaxf(mc[2], mc[3]), top2_merge(mc[2], mc2[2], mc[3], mc2[3]));
-  // The argmax of chain c is tracked as k = 4 tm + r / 4 (o = 8 k + c), a small constant that
-  // the select instruction takes inline; kNoK marks "not seen".
-  constexpr int kNoK = 4 * TM;
+  if (kTop2) {
+    float x = top2_merge(fmaxf(mc[0], mc[1]), top2_merge(mc[0], mc2[0], mc[1], mc2[1]),
+                         fmaxf(mc[2], mc[3]), top2_merge(mc[2], mc2[2], mc[3], mc2[3]));
+    x = top2_shfl_merge(m, x, 16);
+    *m2 = top2_shfl_merge(fmaxf(m, __shfl_xor(m, 16)), x, 32);
+  }
+  float M = fmaxf(m, __shfl_xor(m, 16));
+  M = fmaxf(M, __shfl_xor(M, 32));
+  constexpr int kNoK = TM;  // "not seen"
   float sc[4] = {0.f, 0.f, 0.f, 0.f}, tc[4] = {0.f, 0.f, 0.f, 0.f};
   int32_t kc[4] = {kNoK, kNoK, kNoK, kNoK};
 #pragma unroll
   for (int tm = TM - 1; tm >= 0; --tm)
 #pragma unroll
-    for (int r = 15; r >= 0; --r) {
-      const int o = tm * 32 + 8 * (r >> 2) + (r & 3);
-      const int k = 4 * tm + (r >> 2);
+    for (int r = 3; r >= 0; --r) {
       const float z = acc[tm][tn][r];
       if (kFull) {
-        const float y = (z - m) * kLog2e;
+        const float y = (z - M) * kLog2e;
         const float e = fast_exp2(y);
-        sc[r & 3] += e;
-        tc[r & 3] = fmaf(e, y, tc[r & 3]);
-        kc[r & 3] = z == m ? k : kc[r & 3];
+        sc[r] += e;
+        tc[r] = fmaf(e, y, tc[r]);
+        kc[r] = z == M ? tm : kc[r];
       } else {
-        const bool ok = vbase + o < vocab;
-        // rows past the vocabulary contribute e = 0 and y = 0 (a lane with no valid row keeps
-        // m = kNegBig, where z - m would overflow and 0 * inf would poison t)
-        const float y = ok ? (z - m) * kLog2e : 0.f;
+        // rows past the vocabulary contribute e = 0 and y = 0 (with no valid row in the
+        // column, M = kNegBig, where z - M would overflow and 0 * inf would poison t)
+        const bool ok = vbase + tm * 16 + r < vocab;
+        const float y = ok ? (z - M) * kLog2e : 0.f;
         const float e = ok ? fast_exp2(y) : 0.f;
-        sc[r & 3] += e;
-        tc[r & 3] = fmaf(e, y, tc[r & 3]);
-        kc[r & 3] = (ok && z == m) ? k : kc[r & 3];
+        sc[r] += e;
+        tc[r] = fmaf(e, y, tc[r]);
+        kc[r] = (ok && z == M) ? tm : kc[r];
       }
     }
   int32_t ob = kNoIndex;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) ob = min(ob, kc[c] == kNoK ? kNoIndex : 8 * kc[c] + c);
-  return Partial{m, (sc[0] + sc[1]) + (sc[2] + sc[3]), (tc[0] + tc[1]) + (tc[2] + tc[3]),
-                 ob == kNoIndex ? kNoIndex : vbase + ob};
+  for (int c = 0; c < 4; ++c) ob = min(ob, kc[c] == kNoK ? kNoIndex : 16 * kc[c] + c);
+  int32_t idx = ob == kNoIndex ? kNoIndex : vbase + ob;
+  float s = (sc[0] + sc[1]) + (sc[2] + sc[3]), t = (tc[0] + tc[1]) + (tc[2] + tc[3]);
+  s += __shfl_xor(s, 16);
+  t += __shfl_xor(t, 16);
+  idx = min(idx, __shfl_xor(idx, 16));
+  s += __shfl_xor(s, 32);
+  t += __shfl_xor(t, 32);
+  idx = min(idx, __shfl_xor(idx, 32));
+  return Partial{M, s, t, idx};
 }
 
-// column_partial with the bounds test only where the tile reaches past the vocabulary.
+// column_stats16 with the bounds test only where the tile reaches past the vocabulary.
 template <int TM, int TN, bool kTop2>
-__device__ __forceinline__ Partial column_partial(const f32x16 (&acc)[TM][TN], int tn, int vbase,
+__device__ __forceinline__ Partial column_stats16(const f32x4 (&acc)[TM][TN], int tn, int vbase,
                                                   int vocab, bool full, float* m2) {
-  return full ? column_partial<TM, TN, kTop2, true>(acc, tn, vbase, vocab, m2)
-              : column_partial<TM, TN, kTop2, false>(acc, tn, vbase, vocab, m2);
+  return full ? column_stats16<TM, TN, kTop2, true>(acc, tn, vbase, vocab, m2)
+              : column_stats16<TM, TN, kTop2, false>(acc, tn, vbase, vocab, m2);
 }
 
 // Tile (vt, rt) of position s of the launch sequence: bands of kBand vocabulary tiles (the last
@@ -476,16 +511,17 @@ __device__ __forceinline__ void band_tile(int s, int n_vtiles, int n_rtiles, int
 // its 32 resident workgroups share a few W and h tiles in its L2.  With fewer tiles than
 // workgroups, workgroup g computes tile g.
 //
-// Per tile: 4 waves form a 2 x 2 grid of 128 x 128 sub-tiles (4 x 4 blocks of 32x32x16 MFMAs,
-// 256 accumulator registers per lane).  Per 32-column k step a wave reads 16 KB of operand
-// fragments from LDS; the fragments of the two 16-column halves of a step are double-buffered
-// in registers: the reads of one half are issued before the MFMAs of the other, so LDS latency
-// hides under 16 MFMAs.  The DMA ring keeps RING stages occupied: right after the barrier that
-// ends the reads of stage kt, stage kt + RING is issued into its slot.  When the hidden size
-// spans at least RING stages, the stages issued in the last iterations of a tile are the first
-// stages of the workgroup's next tile (the ring slot of a stage is its index in the workgroup's
-// whole sequence modulo RING), so the next tile's operands arrive while this tile finishes and
-// runs its epilogue.
+// Per tile: 4 waves form a 2 x 2 grid of 128 x 128 sub-tiles, each 8 x 8 blocks of 16x16x32 bf16
+// MFMAs (256 accumulator registers per lane).  A 32-column ring stage is one MFMA k step: per
+// stage a wave reads 16 fragments (16 KB) from LDS and issues 64 MFMAs.  Step kt: one barrier
+// (stage kt + 1 has landed, and every wave's reads of stage kt are done), then the 64 MFMAs of
+// stage kt from one register set while the fragments of stage kt + 1 go into the other and
+// stage kt + RING is loaded into the slot of stage kt; groups of six MFMAs carry one load into
+// LDS and two fragment reads, so both are spread over the step.  The ring slot of a stage is its
+// index in the workgroup's whole sequence modulo RING, so the last steps of a tile issue the
+// next tile's first stages and read its stage 0: its operands arrive while this tile finishes
+// and runs its epilogue.  Measured against 32x32x16 blocks (the same tiles and ring): 16x16x32
+// MFMAs sustain a higher clock under the chip's power limit.
 template <int BM, int RING, bool kTop2>
 __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w, int n_rows, int hidden,
@@ -494,14 +530,17 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
   constexpr int BN = kTileBN, BK = kTileBK;
   constexpr int WM = 2, WN = 2, kWaves = WM * WN;
   constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
-  constexpr int TM = kWaveM / 32, TN = kWaveN / 32;
+  constexpr int TM = kWaveM / 16, TN = kWaveN / 16;
   constexpr int kRowB = BK * 2;                   // 64 bytes per LDS row
   constexpr int kStageBytes = (BM + BN) * kRowB;  // 32 KB
   constexpr int kInst = (BM + BN) / 16;           // 1 KB wave instructions per stage
   constexpr int kInstPerWave = kInst / kWaves;    // 8
   constexpr int kRedBytes = WM * BN * (sizeof(Partial) + 4);
-  static_assert(RING >= 2 && RING <= 4, "ring of 2 to 4 stages");
+  constexpr int kReads = TM + TN, kMfmas = TM * TN;
+  static_assert(RING == 4, "ring of 4 stages (steps go in pairs, and RING - 1 stages in flight)");
+  static_assert(BK == 32, "one 16x16x32 k step per stage");
   static_assert(kInst % kWaves == 0, "stage loads split evenly over the waves");
+  static_assert(6 * kInstPerWave <= kMfmas && kReads == 2 * kInstPerWave, "interleave pattern");
   static_assert(RING * kStageBytes + kRedBytes <= 160 * 1024, "ring and reduction fit in LDS");
   static_assert((RING - 1) * kInstPerWave < 64, "vmcnt range");
   __shared__ __attribute__((aligned(16))) uint8_t smem[RING * kStageBytes + kRedBytes];
@@ -520,8 +559,8 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
-  const int half = lane >> 5, l32 = lane & 31;
-  const int nk = hidden / BK;    // >= 2 (hidden is a multiple of 64)
+  const int q4 = lane >> 4, l16 = lane & 15;
+  const int nk = hidden / BK;     // even (hidden is a multiple of 64), >= 2
   const bool chain = nk >= RING;  // the tail of a tile issues the next tile's first stages
 
   // Load instruction i of this wave covers tile rows 16 q .. 16 q + 15, q = wave * 8 + i (rows
@@ -552,6 +591,15 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
       d.off[i] = static_cast<uint32_t>(r * hidden * 2 + chunk * 16);
     }
   };
+  // A source chosen by value, field by field (a conditional reference to one of two sources
+  // makes the compiler take their addresses and keep them in scratch memory).
+  auto pick = [&](bool c, const Src& x, const Src& y) {
+    Src r;
+    r.rs = c ? x.rs : y.rs;
+#pragma unroll
+    for (int i = 0; i < kInstPerWave; ++i) r.off[i] = c ? x.off[i] : y.off[i];
+    return r;
+  };
   // Stage `stage` of the tile described by d, into ring slot `slot`.
   auto issue = [&](const Src& d, int stage, int slot) {
     uint8_t* base = smem + slot * kStageBytes;
@@ -559,30 +607,22 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
     for (int i = 0; i < kInstPerWave; ++i)
       buffer_load_to_lds(d.rs, base + (wave * kInstPerWave + i) * 1024, d.off[i], stage * BK * 2);
   };
-  // Fragments of half s (k columns 16 s .. 16 s + 15 of the stage in ring slot `slot`, chunk
-  // 2 half + s per lane).
-  auto read = [&](int slot, int s, bf16x8 (&a)[TM], bf16x8 (&b)[TN]) {
+  // Fragment f of a stage (f < TM: W block f of this wave, else h block f - TM): lane l reads
+  // row l % 16 of the 16-row block, 16-byte chunk l / 16 (k = 8 (l / 16) .. + 7).  The 16 lanes
+  // reading one chunk of 16 consecutive rows hit 16 distinct 16-byte bank groups.
+  auto frag = [&](const uint8_t* st, int f) {
+    const int r = f < TM ? wm * kWaveM + f * 16 + l16 : BM + wn * kWaveN + (f - TM) * 16 + l16;
+    return *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (q4 ^ ((r >> 2) & 3)));
+  };
+  auto read = [&](int slot, bf16x8 (&a)[TM], bf16x8 (&b)[TN]) {
     const uint8_t* st = smem + slot * kStageBytes;
-    const int c = 2 * half + s;
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      const int r = wm * kWaveM + tm * 32 + l32;
-      a[tm] = *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (c ^ ((r >> 2) & 3)));
-    }
+    for (int f = 0; f < TM; ++f) a[f] = frag(st, f);
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
-      const int r = BM + wn * kWaveN + tn * 32 + l32;
-      b[tn] = *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (c ^ ((r >> 2) & 3)));
-    }
+    for (int f = 0; f < TN; ++f) b[f] = frag(st, TM + f);
   };
 
-  f32x16 acc[TM][TN];
-  auto mma = [&](const bf16x8 (&a)[TM], const bf16x8 (&b)[TN]) {
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32(a[tm], b[tn], acc[tm][tn]);
-  };
+  f32x4 acc[TM][TN];
   Partial* red = reinterpret_cast<Partial*>(smem + RING * kStageBytes);  // [WM][BN]
   float* red2 = reinterpret_cast<float*>(red + WM * BN);
 
@@ -593,8 +633,9 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
   int slot0 = 0;  // ring slot of the current tile's stage 0
 #pragma unroll
   for (int j = 0; j < RING; ++j) issue(src, min(j, nk - 1), j);
-  constexpr int kReads = TM + TN, kMfmas = TM * TN;
-  static_assert(kInstPerWave + kReads <= kMfmas, "loads and reads interleave with the MFMAs");
+  bf16x8 xa[TM], xb[TN], ya[TM], yb[TN];
+  wait_vm_lds_and_barrier<(RING - 1) * kInstPerWave>();  // stage 0 has landed
+  read(0, xa, xb);
   for (;;) {
     const int ns = s + step;
     const bool next = ns < s_end;
@@ -606,84 +647,63 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
     const bool pre = next && chain;
     auto slot = [&](int kt) { return (slot0 + kt) % RING; };
 
+    // Step kt: the barrier, stage `stage` of p into the slot of stage kt, the fragments of
+    // stage kt + 1 into (na, nb) and the MFMAs of stage kt from (ca, cb).  Every step issues
+    // exactly one stage, so RING - 2 younger stages are in flight at each barrier.
+    auto body = [&](int kt, const Src& p, int stage, const bf16x8 (&ca)[TM],
+                    const bf16x8 (&cb)[TN], bf16x8 (&na)[TM], bf16x8 (&nb)[TN]) {
+      wait_vm_lds_and_barrier<(RING - 2) * kInstPerWave>();
+      uint8_t* lbase = smem + slot(kt) * kStageBytes;
+      const uint8_t* rbase = smem + slot(kt + 1) * kStageBytes;
+#pragma unroll
+      for (int i = 0; i < kMfmas; ++i) {
+        mfma16_tied(acc[i / TN][i % TN], ca[i / TN], cb[i % TN]);
+        if (i < 6 * kInstPerWave) {
+          const int grp = i / 6, r = i % 6;
+          if (r == 1)
+            buffer_load_to_lds(p.rs, lbase + (wave * kInstPerWave + grp) * 1024, p.off[grp],
+                               stage * BK * 2);
+          if (r == 3 || r == 5) {
+            const int f = 2 * grp + (r == 5);
+            if (f < TM)
+              na[f] = frag(rbase, f);
+            else
+              nb[f - TM] = frag(rbase, f);
+          }
+        }
+      }
+    };
 #pragma unroll
     for (int a = 0; a < TM; ++a)
 #pragma unroll
-      for (int b = 0; b < TN; ++b) acc[a][b] = f32x16{};
-    // Every iteration issues exactly one stage (this tile's stage kt + RING, else the next
-    // tile's, else this tile's last stage again into the slot just freed, never read), so the
-    // number of younger stages in flight at each barrier is always RING - 2 and every wait is
-    // the same; straight-line code lets the fragment reads of one half stay in flight under the
-    // MFMAs of the other.
-    wait_vm_lds_and_barrier<(RING - 1) * kInstPerWave>();  // stage 0 has landed
-    bf16x8 xa[TM], xb[TN], ya[TM], yb[TN];
-    read(slot(0), 0, xa, xb);
-    // Step kt: half 1 of stage kt, the barrier, then stage `stage` of the tile at p into the
-    // slot of stage kt + RING (the slot stage kt just freed) and half 2 of stage kt.
-    auto body = [&](int kt, const Src& p, int stage) {
-      read(slot(kt), 1, ya, yb);
-      mma(xa, xb);
-      // one fragment read after each of the first kReads MFMAs
-#pragma unroll
-      for (int i = 0; i < kReads; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfmas - kReads, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      wait_vm_lds_and_barrier<(RING - 2) * kInstPerWave>();  // stage kt + 1 has landed
-      issue(p, stage, slot(kt + RING));
-      read(slot(kt + 1), 0, xa, xb);
-      mma(ya, yb);
-      // one DMA load after each of the first kInstPerWave MFMAs, one fragment read after each
-      // of the next kReads
-#pragma unroll
-      for (int i = 0; i < kInstPerWave; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
-      }
-#pragma unroll
-      for (int i = 0; i < kReads; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      if constexpr (kMfmas > kInstPerWave + kReads)
-        __builtin_amdgcn_sched_group_barrier(0x008, kMfmas - kInstPerWave - kReads, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    };
-    // Every step issues exactly one stage: this tile's stage kt + RING while there is one,
-    // then the next tile's first stages (or, without a next tile or with fewer than RING
-    // stages per tile, this tile's last stage again into the slot just freed, never read).  So
-    // the number of younger stages in flight at each barrier is always RING - 2 and every wait
-    // is the same; straight-line steps let the fragment reads of one half stay in flight under
-    // the MFMAs of the other.
+      for (int b = 0; b < TN; ++b) acc[a][b] = f32x4{};
+    acc_fence_in(acc);  // the zeros are in place before the first MFMA reads them
+    // Steps go in pairs, alternating the two register sets (nk and RING are even, so a pair
+    // never straddles the end of this tile's stages).  Once this tile has no stage kt + RING,
+    // a step issues the next tile's first stages (or, without a next tile or with fewer than
+    // RING stages per tile, this tile's last stage again into the slot just freed, never read).
+    const Src tsrc = pick(pre, nsrc, src);
     int kt = 0;
-    for (; kt + RING < nk; ++kt) body(kt, src, kt + RING);
-    const Src& tsrc = pre ? nsrc : src;
-    for (; kt + 1 < nk; ++kt) body(kt, tsrc, pre ? kt + RING - nk : nk - 1);
-    read(slot(nk - 1), 1, ya, yb);
-    mma(xa, xb);
-    mma(ya, yb);
-    if (pre) {
-      // every wave is done reading the ring; the next tile's stage RING - 1 goes into the slot
-      // of this tile's last stage (its stages 0 .. RING - 2 are in flight already)
-      wait_vm_lds_and_barrier<63>();
-      issue(nsrc, RING - 1, slot(nk + RING - 1));
-    } else {
-      wait_vm_lds_and_barrier<0>();  // no DMA in flight; every wave is done reading the ring
+    for (; kt + RING < nk; kt += 2) {
+      body(kt, src, kt + RING, xa, xb, ya, yb);
+      body(kt + 1, src, kt + 1 + RING, ya, yb, xa, xb);
     }
+    for (; kt < nk; kt += 2) {
+      body(kt, tsrc, pre ? kt + RING - nk : nk - 1, xa, xb, ya, yb);
+      body(kt + 1, tsrc, pre ? kt + 1 + RING - nk : nk - 1, ya, yb, xa, xb);
+    }
+    if (!pre) wait_vm_lds_and_barrier<0>();  // no DMA in flight
+    acc_fence_out(acc);  // every MFMA has written its accumulator before the epilogue reads it
 
     const bool full = vt * BM + BM <= vocab;
-    const int vbase = vt * BM + wm * kWaveM + 4 * half;
+    const int vbase = vt * BM + wm * kWaveM + 4 * q4;
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
       float m2 = kNegBig;
-      Partial p = column_partial<TM, TN, kTop2>(acc, tn, vbase, vocab, full, &m2);
-      if (kTop2) m2 = top2_shfl_merge(p.m, m2, 32);
-      p = partial_xor_merge(p, 32, lane);
-      if (lane < 32) {
-        red[wm * BN + wn * kWaveN + tn * 32 + l32] = p;
-        if (kTop2) red2[wm * BN + wn * kWaveN + tn * 32 + l32] = m2;
+      const Partial p = column_stats16<TM, TN, kTop2>(acc, tn, vbase, vocab, full, &m2);
+      if (lane < 16) {
+        red[wm * BN + wn * kWaveN + tn * 16 + l16] = p;
+        if (kTop2) red2[wm * BN + wn * kWaveN + tn * 16 + l16] = m2;
       }
     }
     __syncthreads();
@@ -708,21 +728,24 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
     rt = nrt;
     src = nsrc;
     if (pre) {
-      slot0 = (slot0 + nk) % RING;
+      slot0 = (slot0 + nk) % RING;  // stage 0 of this tile is in xa, xb already
     } else {
       slot0 = 0;
+      __syncthreads();  // every wave is done with the ring
 #pragma unroll
       for (int j = 0; j < RING; ++j) issue(src, min(j, nk - 1), j);
+      wait_vm_lds_and_barrier<(RING - 1) * kInstPerWave>();
+      read(0, xa, xb);
     }
   }
 }
 
 // Tile kernel of the large-batch path: 256 x 256 tiles, 4 waves of 128 x 128, ring of 4
 // (128 KB LDS, one workgroup per compute unit).
-// Measured and dropped: 8 waves of 128 x 64 (10.55 ms), 256 x 128 tiles with a ring of 3 at two
-// workgroups per compute unit (11.8 ms), stages reaching LDS through registers (9.65 ms),
-// 64-column stages with one barrier per 64 MFMAs (10.1 ms), DMA loads spread over both halves of
-// a step (no change), 384 x 256 tiles (384 accumulators per lane: the compiler spills).
+// Measured and dropped (with 32x32x16 blocks): 8 waves of 128 x 64 (10.55 ms), 256 x 128 tiles
+// with a ring of 3 at two workgroups per compute unit (11.8 ms), stages reaching LDS through
+// registers (9.65 ms), 64-column stages with one barrier per 64 MFMAs (10.1 ms), 384 x 256 tiles
+// (384 accumulators per lane: the compiler spills).
 template <bool kTop2>
 hipError_t launch_tile(int n_rows, int hidden, int vocab, const void* h, const void* w,
                        Partial* part, float* part2, hipStream_t s) {
