@@ -363,8 +363,8 @@ hipError_t launch_stream_rows(int n_rows, int hidden, int vocab, const void* h, 
 // 16 bytes to LDS base + 16 l) into a ring of RING stages of BK = 32 hidden columns, RING - 1
 // stages in flight; no staging registers and no LDS store instructions.  LDS rows are 64 bytes
 // without padding; the 16-byte chunk c of row r is kept in slot c ^ ((r / 4) % 4), which makes
-// the 16-row MFMA operand reads free of bank conflicts.  Four waves form a 2 x 2 grid of
-// 128 x 128 sub-tiles of 16x16x32 MFMA blocks.
+// the 16-row MFMA operand reads (rows in the order rho of lmhead_tile_kernel) free of bank
+// conflicts.  Four waves form a 2 x 2 grid of 128 x 128 sub-tiles of 16x16x32 MFMA blocks.
 //
 // Tile order is XCD-aware: the launch sequence takes vocabulary tiles in bands of kBand, each
 // band swept position tile by position tile, and is cut into one contiguous segment per XCD
@@ -412,8 +412,9 @@ __device__ __forceinline__ void acc_fence_out(f32x4 (&acc)[TM][TN]) {
 }
 
 // Statistics of one column of a wave's 16x16x32 accumulator tile: lane l holds, for column block
-// tn, vocabulary rows vbase + 16 tm + r (tm < TM, r < 4; vbase includes the lane's 4 (l / 16)) of
-// column l % 16, and the four lanes l % 16 + 16 q together hold the column's 16 TM rows.  A max
+// tn, vocabulary rows vbase + 16 tm + 4 r (tm < TM, r < 4; vbase includes the lane's l / 16) of
+// one column, and the four lanes l % 16 + 16 q together hold the column's 16 TM rows (the rows
+// of a 16-row block reach the MFMA in the order the fragment reads use, see lmhead_tile_kernel).  A max
 // pass in four chains (by r), the column maximum M over the four lanes, one exponential pass
 // against M, then the four lanes' sums added by a butterfly (a + b on one lane, b + a on its
 // partner: identical bits on all four).  Each chain walks its rows in decreasing order, so its
@@ -429,7 +430,7 @@ __device__ __forceinline__ Partial column_stats16(const f32x4 (&acc)[TM][TN], in
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      if (kFull || vbase + tm * 16 + r < vocab) {
+      if (kFull || vbase + tm * 16 + 4 * r < vocab) {
         const float z = acc[tm][tn][r];
         // with mc >= mc2, the new second-largest is the median of (mc, mc2, z): one v_med3
         if (kTop2) mc2[r] = __builtin_amdgcn_fmed3f(mc[r], mc2[r], z);
@@ -462,7 +463,7 @@ __device__ __forceinline__ Partial column_stats16(const f32x4 (&acc)[TM][TN], in
       } else {
         // rows past the vocabulary contribute e = 0 and y = 0 (with no valid row in the
         // column, M = kNegBig, where z - M would overflow and 0 * inf would poison t)
-        const bool ok = vbase + tm * 16 + r < vocab;
+        const bool ok = vbase + tm * 16 + 4 * r < vocab;
         const float y = ok ? (z - M) * kLog2e : 0.f;
         const float e = ok ? fast_exp2(y) : 0.f;
         sc[r] += e;
@@ -472,7 +473,7 @@ __device__ __forceinline__ Partial column_stats16(const f32x4 (&acc)[TM][TN], in
     }
   int32_t ob = kNoIndex;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) ob = min(ob, kc[c] == kNoK ? kNoIndex : 16 * kc[c] + c);
+  for (int c = 0; c < 4; ++c) ob = min(ob, kc[c] == kNoK ? kNoIndex : 16 * kc[c] + 4 * c);
   int32_t idx = ob == kNoIndex ? kNoIndex : vbase + ob;
   float s = (sc[0] + sc[1]) + (sc[2] + sc[3]), t = (tc[0] + tc[1]) + (tc[2] + tc[3]);
   s += __shfl_xor(s, 16);
@@ -608,10 +609,15 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
       buffer_load_to_lds(d.rs, base + (wave * kInstPerWave + i) * 1024, d.off[i], stage * BK * 2);
   };
   // Fragment f of a stage (f < TM: W block f of this wave, else h block f - TM): lane l reads
-  // row l % 16 of the 16-row block, 16-byte chunk l / 16 (k = 8 (l / 16) .. + 7).  The 16 lanes
-  // reading one chunk of 16 consecutive rows hit 16 distinct 16-byte bank groups.
+  // row rho(l % 16) = 4 (l % 4) + (l % 16) / 4 of the 16-row block, 16-byte chunk l / 16
+  // (k = 8 (l / 16) .. + 7).  Rows in their natural order (lane l, row l % 16) make every read a
+  // 2-way LDS bank conflict (rocprofv3 SQ_LDS_BANK_CONFLICT: 4 extra cycles per read, none with
+  // rho).  The MFMA then sees the block's rows permuted by rho, on both operands: accumulator
+  // register r of lane l holds vocabulary row 16 tm + rho(4 (l / 16) + r) = 16 tm + 4 r + l / 16
+  // of the wave's W rows, for position tn * 16 + rho(l % 16) of its h rows.
+  const int rho = 4 * (l16 & 3) + (l16 >> 2);
   auto frag = [&](const uint8_t* st, int f) {
-    const int r = f < TM ? wm * kWaveM + f * 16 + l16 : BM + wn * kWaveN + (f - TM) * 16 + l16;
+    const int r = f < TM ? wm * kWaveM + f * 16 + rho : BM + wn * kWaveN + (f - TM) * 16 + rho;
     return *reinterpret_cast<const bf16x8*>(st + r * kRowB + 16 * (q4 ^ ((r >> 2) & 3)));
   };
   auto read = [&](int slot, bf16x8 (&a)[TM], bf16x8 (&b)[TN]) {
@@ -696,14 +702,14 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
     acc_fence_out(acc);  // every MFMA has written its accumulator before the epilogue reads it
 
     const bool full = vt * BM + BM <= vocab;
-    const int vbase = vt * BM + wm * kWaveM + 4 * q4;
+    const int vbase = vt * BM + wm * kWaveM + q4;
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
       float m2 = kNegBig;
       const Partial p = column_stats16<TM, TN, kTop2>(acc, tn, vbase, vocab, full, &m2);
       if (lane < 16) {
-        red[wm * BN + wn * kWaveN + tn * 16 + l16] = p;
-        if (kTop2) red2[wm * BN + wn * kWaveN + tn * 16 + l16] = m2;
+        red[wm * BN + wn * kWaveN + tn * 16 + rho] = p;
+        if (kTop2) red2[wm * BN + wn * kWaveN + tn * 16 + rho] = m2;
       }
     }
     __syncthreads();
