@@ -558,7 +558,10 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
   }
   if (s0 >= s_end) return;  // whole workgroup
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index is the same on every lane: taken as a scalar, so the LDS destinations of the
+  // loads (M0) are scalar arithmetic
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % WM, wn = wave / WM;
   const int q4 = lane >> 4, l16 = lane & 15;
   const int nk = hidden / BK;     // even (hidden is a multiple of 64), >= 2
@@ -573,7 +576,7 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
   // count on the LDS-read counter as well, and the compiler then waits for every outstanding
   // fragment read before each use of one.)
   static_assert((BM / 16) % kInstPerWave == 0, "a wave loads from one operand");
-  const bool w_wave = __builtin_amdgcn_readfirstlane(wave) * kInstPerWave * 16 < BM;
+  const bool w_wave = wave * kInstPerWave * 16 < BM;
   struct Src {
     __amdgpu_buffer_rsrc_t rs;
     uint32_t off[kInstPerWave];
@@ -651,7 +654,7 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
       set_src(nsrc, nvt, nrt);
     }
     const bool pre = next && chain;
-    auto slot = [&](int kt) { return (slot0 + kt) % RING; };
+    auto slot = [&](int kt) { return static_cast<int>(static_cast<unsigned>(slot0 + kt) % RING); };
 
     // Step kt: the barrier, stage `stage` of p into the slot of stage kt, the fragments of
     // stage kt + 1 into (na, nb) and the MFMAs of stage kt from (ca, cb).  Every step issues
