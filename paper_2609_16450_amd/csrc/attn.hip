@@ -536,21 +536,35 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_d128_kernel(AttnParams 
 #pragma unroll
     for (int m = 0; m < kPreK; ++m) kf[m] = kread(m);
     __builtin_amdgcn_sched_barrier(0);
-    // S(st + 1), each MFMA followed by one word of P(st): registers 8u + 2e, 8u + 2e + 1 of
-    // scur[kb] are keys kb*32 + 16u + 4 half + ... -- exactly the B operand layout of P V
+    // S(st + 1), each MFMA followed by the P(st) work of one slot: registers 8u + 2e, 8u + 2e + 1
+    // of scur[kb] are keys kb*32 + 16u + 4 half + ... -- exactly the B operand layout of P V.
+    // The P words are software-pipelined over the slots: slot m forms the exponents of word
+    // m + 1, the exponentials of word m and the bf16 pair and running sum of word m - 1, so an
+    // instruction does not wait on the one just before it (a wave issues in order).
+    auto expo = [&](int w, float (&y)[2]) {
+      const int kb = w / 8, u = (w / 4) % 2, e = w % 4;
+      y[0] = fmaf(scur[kb][8 * u + 2 * e], p.scale_log2, -m_run);
+      y[1] = fmaf(scur[kb][8 * u + 2 * e + 1], p.scale_log2, -m_run);
+    };
+    float ya[2][2], ea[2][2];
+    auto commit = [&](int w) {
+      const uint32_t wd = pack2_bf16(ea[w & 1][0], ea[w & 1][1]);
+      pw[w / 4][w % 4] = wd;
+      lsum = sum2_bf16(wd, lsum);
+    };
+    expo(0, ya[0]);
 #pragma unroll
     for (int m = 0; m < kMfmas; ++m) {
       if (m + kPreK < kMfmas) kf[m + kPreK] = kread(m + kPreK);
       if (m >= kMfmas - kPreV) vf[m - (kMfmas - kPreV)] = vread(m - (kMfmas - kPreV));
       snxt[m % kKB] = mfma32(kf[m], qf[m / kKB], snxt[m % kKB]);
-      const int kb = m / 8, u = (m / 4) % 2, e = m % 4;
-      const uint32_t w =
-          pack2_bf16(fast_exp2(fmaf(scur[kb][8 * u + 2 * e], p.scale_log2, -m_run)),
-                     fast_exp2(fmaf(scur[kb][8 * u + 2 * e + 1], p.scale_log2, -m_run)));
-      pw[m / 4][e] = w;
-      lsum = sum2_bf16(w, lsum);
+      if (m + 1 < kMfmas) expo(m + 1, ya[(m + 1) & 1]);
+      ea[m & 1][0] = fast_exp2(ya[m & 1][0]);
+      ea[m & 1][1] = fast_exp2(ya[m & 1][1]);
+      if (m >= 1) commit(m - 1);
       __builtin_amdgcn_sched_barrier(0);
     }
+    commit(kMfmas - 1);
     // O^T += V^T P^T, each MFMA followed by a step of the maximum of S(st + 1)
     float mx[2] = {-INFINITY, -INFINITY};
 #pragma unroll
