@@ -411,16 +411,55 @@ __device__ __forceinline__ void acc_fence_out(f32x4 (&acc)[TM][TN]) {
     for (int b = 0; b < TN; ++b) asm volatile("" : "+a"(acc[a][b]));
 }
 
+// Reductions over the four lanes l % 16 + 16 q (q < 4) of a column, in registers: the gfx950
+// swaps v_permlane16_swap / v_permlane32_swap hand every lane the values of the lower and upper
+// lane of its pair (l & ~16 and l | 16, then l & ~32 and l | 32), which are combined as
+// lower op upper, so both lanes of a pair evaluate the same expression and end with the same
+// bits.
+__device__ __forceinline__ void lane_pair16(float x, float& lo, float& hi) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void lane_pair32(float x, float& lo, float& hi) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair_max(float m) {
+  float lo, hi;
+  lane_pair16(m, lo, hi);
+  m = fmaxf(lo, hi);
+  lane_pair32(m, lo, hi);
+  return fmaxf(lo, hi);
+}
+__device__ __forceinline__ void pair_sum_min(float& s, float& t, int32_t& idx) {
+  float lo, hi, lo2, hi2, lo3, hi3;
+  lane_pair16(s, lo, hi);
+  lane_pair16(t, lo2, hi2);
+  lane_pair16(__int_as_float(idx), lo3, hi3);
+  s = lo + hi;
+  t = lo2 + hi2;
+  idx = min(__float_as_int(lo3), __float_as_int(hi3));
+  lane_pair32(s, lo, hi);
+  lane_pair32(t, lo2, hi2);
+  lane_pair32(__int_as_float(idx), lo3, hi3);
+  s = lo + hi;
+  t = lo2 + hi2;
+  idx = min(__float_as_int(lo3), __float_as_int(hi3));
+}
+
 // Statistics of one column of a wave's 16x16x32 accumulator tile: lane l holds, for column block
 // tn, vocabulary rows vbase + 16 tm + 4 r (tm < TM, r < 4; vbase includes the lane's l / 16) of
 // one column, and the four lanes l % 16 + 16 q together hold the column's 16 TM rows (the rows
-// of a 16-row block reach the MFMA in the order the fragment reads use, see lmhead_tile_kernel).  A max
-// pass in four chains (by r), the column maximum M over the four lanes, one exponential pass
-// against M, then the four lanes' sums added by a butterfly (a + b on one lane, b + a on its
-// partner: identical bits on all four).  Each chain walks its rows in decreasing order, so its
-// last z == M is its lowest row; the argmax is kept as the block index tm, a constant of the
-// unrolled code.  kFull (every row inside the vocabulary) drops the per-row bounds test.  With
-// kTop2, m2 returns the column's second-largest logit (kNegBig if none).
+// of a 16-row block reach the MFMA in the order the fragment reads use, see
+// lmhead_tile_kernel).  A max pass in four chains (by r), the column maximum M over the four
+// lanes (pair_max), one exponential pass against M, then the four lanes' sums added pairwise in
+// registers (pair_sum_min): identical bits on all four lanes.  Each chain walks its rows in
+// decreasing order, so its last z == M is its lowest row; the argmax is kept as the block index
+// tm, a constant of the unrolled code.  kFull (every row inside the vocabulary) drops the
+// per-row bounds test.  With kTop2, m2 returns the column's second-largest logit (kNegBig if
+// none).
 template <int TM, int TN, bool kTop2, bool kFull>
 __device__ __forceinline__ Partial column_stats16(const f32x4 (&acc)[TM][TN], int tn, int vbase,
                                                   int vocab, float* m2) {
@@ -444,8 +483,7 @@ __device__ __forceinline__ Partial column_stats16(const f32x4 (&acc)[TM][TN], in
     x = top2_shfl_merge(m, x, 16);
     *m2 = top2_shfl_merge(fmaxf(m, __shfl_xor(m, 16)), x, 32);
   }
-  float M = fmaxf(m, __shfl_xor(m, 16));
-  M = fmaxf(M, __shfl_xor(M, 32));
+  float M = pair_max(m);
   constexpr int kNoK = TM;  // "not seen"
   float sc[4] = {0.f, 0.f, 0.f, 0.f}, tc[4] = {0.f, 0.f, 0.f, 0.f};
   int32_t kc[4] = {kNoK, kNoK, kNoK, kNoK};
@@ -476,12 +514,7 @@ __device__ __forceinline__ Partial column_stats16(const f32x4 (&acc)[TM][TN], in
   for (int c = 0; c < 4; ++c) ob = min(ob, kc[c] == kNoK ? kNoIndex : 16 * kc[c] + 4 * c);
   int32_t idx = ob == kNoIndex ? kNoIndex : vbase + ob;
   float s = (sc[0] + sc[1]) + (sc[2] + sc[3]), t = (tc[0] + tc[1]) + (tc[2] + tc[3]);
-  s += __shfl_xor(s, 16);
-  t += __shfl_xor(t, 16);
-  idx = min(idx, __shfl_xor(idx, 16));
-  s += __shfl_xor(s, 32);
-  t += __shfl_xor(t, 32);
-  idx = min(idx, __shfl_xor(idx, 32));
+  pair_sum_min(s, t, idx);
   return Partial{M, s, t, idx};
 }
 
