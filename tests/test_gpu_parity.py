@@ -102,18 +102,31 @@ def test_lmhead_small(n_rows, hidden, vocab, dt):
                 ds.max_logit.cpu().numpy(), ref)
 
 
-def test_lmhead_vocab_ties_take_lowest_id():
+# Duplicates of the winning W row.  The large-batch kernel holds vocabulary row 16 tm + 4 r + q
+# of a wave's 128 rows in register r of lane group q, so ids 130 / 134 share a lane and differ
+# in the register chain, 130 / 146 share a chain and differ in the block, 129 / 130 sit in
+# different lanes of one column, and 2999 lies in the last, partial vocabulary tile.
+TIE_CASES = [
+    (40, (130, 2999)),          # streaming kernel (at most 64 positions)
+    (300, (146, 134, 130, 2999)),  # tile kernel: lowest in the same lane, other chain / block
+    (300, (146, 134, 129, 2999)),  # tile kernel: lowest in another lane of the column
+    (300, (2999,)),             # tile kernel: the winner in the partial last tile only
+]
+
+
+@pytest.mark.parametrize("n,dups", TIE_CASES)
+def test_lmhead_vocab_ties_take_lowest_id(n, dups):
     # Duplicate rows of W give bit-identical logits (same accumulation order, no split over the
     # hidden dimension), so the lowest duplicated id must win.
-    say("lmhead ties")
+    say(f"lmhead ties n={n} dups={dups}")
     rng = np.random.default_rng(5)
-    n, d, V = 40, 256, 3000
+    d, V = 256, 3000
     h = torch.from_numpy(rng.standard_normal((n, d)).astype(np.float32)).to(torch.bfloat16).cuda()
     w = torch.from_numpy((rng.standard_normal((V, d)) / 16).astype(np.float32)).to(torch.bfloat16)
-    # make row 2900 the clear winner for every position, then copy it to ids 130 and 2999
+    # make row 2900 the clear winner for every position, then copy it to the duplicate ids
     w[2900] = (h.float().cpu().mean(0) * 4).to(torch.bfloat16)
-    w[130] = w[2900]
-    w[2999] = w[2900]
+    for i in dups:
+        w[i] = w[2900]
     w = w.cuda()
     conf = torch.empty(n, device="cuda")
     ent = torch.empty(n, device="cuda")
@@ -124,7 +137,7 @@ def test_lmhead_vocab_ties_take_lowest_id():
     m = z.max(1)
     winners = [np.flatnonzero(z[i] == m[i])[0] for i in range(n)]
     np.testing.assert_array_equal(am.cpu().numpy(), winners)
-    assert (am.cpu().numpy() == 130).sum() > 0
+    assert (am.cpu().numpy() == min(min(dups), 2900)).sum() > 0
 
 
 # ----------------------------------------------------------------------------------------
