@@ -48,8 +48,9 @@ LM_CASES = [
     (600, 192, 9000, "bf16"),
     (32, 256, 126464, "bf16"),
     (48, 192, 152064, "bf16"),
-    # streaming kernel with the top-2 track: 16 waves of 3 row tiles; 8 waves of 7 and 8
+    # streaming kernel with the top-2 track: 16 waves of 3 and 2 row tiles; 8 waves of 7 and 8
     (17, 128, 152064, "bf16"),
+    (5, 4160, 100003, "bf16"),
     (8, 64, 200000, "bf16"),
     (2, 64, 262144, "bf16"),
     (7, 100, 999, "f32"),

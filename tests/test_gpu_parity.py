@@ -69,8 +69,12 @@ LM_CASES = [
     (300, 128, 70000, "bf16"),
     (1100, 192, 100000, "bf16"),
     (700, 64, 40000, "bf16"),
-    # streaming kernel: 16 waves with 1..3 row tiles each, 8 waves with 7 or 8, partial h chunks
+    # streaming kernel: 16 waves with 1..3 row tiles each, 8 waves with 7 or 8, partial h chunks;
+    # two row tiles per wave with one, two and four position tiles (100003: a partial last slice)
     (32, 256, 126464, "bf16"),
+    (5, 4160, 100003, "bf16"),
+    (20, 64, 100000, "bf16"),
+    (64, 128, 126464, "bf16"),
     (17, 128, 152064, "bf16"),
     (48, 192, 152064, "bf16"),
     (8, 64, 200000, "bf16"),
