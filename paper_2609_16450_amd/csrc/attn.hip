@@ -432,7 +432,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_d128_kernel(AttnParams 
   auto ktile = [&](int i) { return smem + (i & 1) * kTileBytes; };
   auto vtile = [&](int i) { return smem + (2 + (i & 1)) * kTileBytes; };
 
-  // S^T of tile st into acc (unmasked): acc[kb][r] = S[query l32][key kb*32 + 8(r/4) + 4 half + r%4]
+  // S^T of tile st into acc (unmasked):
+  // acc[kb][r] = S[query l32][key kb*32 + 8(r/4) + 4 half + r%4]
   auto scores = [&](int st, f32x16 (&acc)[kKB]) {
     const uint8_t* Kt = ktile(st);
 #pragma unroll
@@ -492,7 +493,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_d128_kernel(AttnParams 
 
   const int q4 = lane & 3, j4 = (lane >> 2) & 3;
   const int d0 = 16 * ((lane >> 4) & 1);
-  for (int st = 0; st < n_stages; ++st) {
+  // Iteration st: S(st + 1) into snxt_ while P(st) comes from scur_.  Two iterations per trip
+  // with the two score arrays swapping roles, so the next tile's scores are never copied.
+  auto step = [&](int st, f32x16 (&scur_)[kKB], f32x16 (&snxt_)[kKB]) {
     // this wave's loads of K(st + 1) and V(st) have landed; after the barrier every wave's
     // have, and every wave is done with K(st) and V(st - 1)
     wait_vm_lds_and_barrier<0>();
@@ -527,9 +530,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_d128_kernel(AttnParams 
       return __builtin_bit_cast(bf16x8,
                                 __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
     };
-    f32x16 snxt[kKB];
 #pragma unroll
-    for (int kb = 0; kb < kKB; ++kb) snxt[kb] = f32x16{};
+    for (int kb = 0; kb < kKB; ++kb) snxt_[kb] = f32x16{};
     bf16x8 kf[kMfmas], vf[kMfmas];
     u32x4 pw[2 * kKB];  // P(st) as bf16 pairs: word e of MFMA group 2 kb + u
     float lsum = 0.f;
@@ -537,14 +539,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_d128_kernel(AttnParams 
     for (int m = 0; m < kPreK; ++m) kf[m] = kread(m);
     __builtin_amdgcn_sched_barrier(0);
     // S(st + 1), each MFMA followed by the P(st) work of one slot: registers 8u + 2e, 8u + 2e + 1
-    // of scur[kb] are keys kb*32 + 16u + 4 half + ... -- exactly the B operand layout of P V.
+    // of scur_[kb] are keys kb*32 + 16u + 4 half + ... -- exactly the B operand layout of P V.
     // The P words are software-pipelined over the slots: slot m forms the exponents of word
     // m + 1, the exponentials of word m and the bf16 pair and running sum of word m - 1, so an
     // instruction does not wait on the one just before it (a wave issues in order).
     auto expo = [&](int w, float (&y)[2]) {
       const int kb = w / 8, u = (w / 4) % 2, e = w % 4;
-      y[0] = fmaf(scur[kb][8 * u + 2 * e], p.scale_log2, -m_run);
-      y[1] = fmaf(scur[kb][8 * u + 2 * e + 1], p.scale_log2, -m_run);
+      y[0] = fmaf(scur_[kb][8 * u + 2 * e], p.scale_log2, -m_run);
+      y[1] = fmaf(scur_[kb][8 * u + 2 * e + 1], p.scale_log2, -m_run);
     };
     float ya[2][2], ea[2][2];
     auto commit = [&](int w) {
@@ -557,7 +559,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_d128_kernel(AttnParams 
     for (int m = 0; m < kMfmas; ++m) {
       if (m + kPreK < kMfmas) kf[m + kPreK] = kread(m + kPreK);
       if (m >= kMfmas - kPreV) vf[m - (kMfmas - kPreV)] = vread(m - (kMfmas - kPreV));
-      snxt[m % kKB] = mfma32(kf[m], qf[m / kKB], snxt[m % kKB]);
+      snxt_[m % kKB] = mfma32(kf[m], qf[m / kKB], snxt_[m % kKB]);
       if (m + 1 < kMfmas) expo(m + 1, ya[(m + 1) & 1]);
       ea[m & 1][0] = fast_exp2(ya[m & 1][0]);
       ea[m & 1][1] = fast_exp2(ya[m & 1][1]);
@@ -572,18 +574,21 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_d128_kernel(AttnParams 
       if (n + kPreV < kMfmas) vf[n + kPreV] = vread(n + kPreV);
       o[n % kDBlocks] =
           mfma32(vf[n], __builtin_bit_cast(bf16x8, pw[n / kDBlocks]), o[n % kDBlocks]);
-      mx[n & 1] = fmaxf(mx[n & 1], fmaxf(snxt[n / 8][2 * (n % 8)], snxt[n / 8][2 * (n % 8) + 1]));
+      mx[n & 1] = fmaxf(mx[n & 1], fmaxf(snxt_[n / 8][2 * (n % 8)], snxt_[n / 8][2 * (n % 8) + 1]));
       asm volatile("" : "+v"(mx[n & 1]));  // keep the step here, between the MFMAs
       __builtin_amdgcn_sched_barrier(0);
     }
     l_run += lsum;
     if (more) {
       float mloc = fmaxf(mx[0], mx[1]);
-      if (kbeg + (st + 2) * kDmaKeys > kend) mloc = mask_max(st + 1, snxt);  // last, partial tile
+      if (kbeg + (st + 2) * kDmaKeys > kend) mloc = mask_max(st + 1, snxt_);  // last, partial tile
       update_max(mloc);
-#pragma unroll
-      for (int kb = 0; kb < kKB; ++kb) scur[kb] = snxt[kb];
     }
+  };
+  f32x16 salt[kKB];
+  for (int st = 0; st < n_stages; st += 2) {
+    step(st, scur, salt);
+    if (st + 1 < n_stages) step(st + 1, salt, scur);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
