@@ -303,7 +303,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p, in
 // iteration, then the 16 MFMAs of O^T += V(st)^T P(st)^T, each followed by one step of the
 // maximum of S(st + 1).  Scheduling barriers keep that interleave, so one wave's exponentials
 // run while its matrix pipe works.  V^T fragments come from transposing LDS reads of the
-// row-major V tile.
+// row-major V tile.  The loop runs two iterations per trip, the score arrays of S(st) and
+// S(st + 1) trading places between them, so no scores are copied.
 //
 // Softmax.  The running maximum m (log2 units) moves only when some row's stage maximum
 // exceeds it by more than kAttnSlack, so probabilities 2^(s - m) stay below 2^kAttnSlack and
