@@ -236,7 +236,8 @@ __device__ __forceinline__ void attn_small_role(const AttnParams& p, int unit, i
   uint16_t* dst = p.out + q_off;
 #pragma unroll
   for (int t = 0; t < kDTiles; ++t) {
-    const u32x2 v{pack2_bf16(o[t][0] * inv, o[t][1] * inv), pack2_bf16(o[t][2] * inv, o[t][3] * inv)};
+    const u32x2 v{pack2_bf16(o[t][0] * inv, o[t][1] * inv),
+                  pack2_bf16(o[t][2] * inv, o[t][3] * inv)};
     *reinterpret_cast<u32x2*>(dst + 16 * t + 4 * grp) = v;
   }
 }

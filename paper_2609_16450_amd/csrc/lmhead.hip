@@ -417,12 +417,14 @@ __device__ __forceinline__ void acc_fence_out(f32x4 (&acc)[TM][TN]) {
 // lower op upper, so both lanes of a pair evaluate the same expression and end with the same
 // bits.
 __device__ __forceinline__ void lane_pair16(float x, float& lo, float& hi) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const auto r =
+      __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   lo = __uint_as_float(r[0]);
   hi = __uint_as_float(r[1]);
 }
 __device__ __forceinline__ void lane_pair32(float x, float& lo, float& hi) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const auto r =
+      __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   lo = __uint_as_float(r[0]);
   hi = __uint_as_float(r[1]);
 }
@@ -616,7 +618,8 @@ __global__ __launch_bounds__(256, 1) void lmhead_tile_kernel(
   };
   auto set_src = [&](Src& d, int vt_, int rt_) {
     const uint16_t* base =
-        w_wave ? w + static_cast<size_t>(vt_) * BM * hidden : h + static_cast<size_t>(rt_) * BN * hidden;
+        w_wave ? w + static_cast<size_t>(vt_) * BM * hidden
+               : h + static_cast<size_t>(rt_) * BN * hidden;
     const int last = w_wave ? vocab - 1 - vt_ * BM : n_rows - 1 - rt_ * BN;  // >= 0
     d.rs = make_rsrc(base);
 #pragma unroll
