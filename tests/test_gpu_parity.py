@@ -531,11 +531,11 @@ def _random_step_spec(i):
                 block_len=("uniform", 0, hi), prefix_len=("uniform", 0, int(r.integers(1, 700))))
 
 
-@pytest.mark.parametrize("i", range(12))
+@pytest.mark.parametrize("i", range(40))
 def test_decode_step_random_shapes(i):
     spec = _random_step_spec(i)
     say(f"decode_step random shape {i}: {spec}")
-    case = make_step(custom_config(f"random{i}", **spec))
+    case = enforce_margins(make_step(custom_config(f"random{i}", **spec)))
     a = DeviceStep(case)
     eb_decode_step(a.buffers)
     b = DeviceStep(case)
@@ -554,6 +554,9 @@ def test_decode_step_random_shapes(i):
         ref = oracle.block_attention(**f, cu_block=case.cu_block, cu_prefix=case.cu_prefix,
                                      hq=spec["hq"], hkv=spec["hkv"])
         np.testing.assert_allclose(attn_out_f32(a.attn_out), ref, **ATTN_TOL_BF16)
+        ref = oracle.lmhead_confidence(as_f32(case.h, "bf16"), as_f32(case.w, "bf16"))
+        check_stats(a.conf.cpu().numpy(), a.entropy.cpu().numpy(), a.argmax.cpu().numpy(),
+                    a.max_logit.cpu().numpy(), ref)
 
 
 class _DebugChecks:
